@@ -1,0 +1,156 @@
+/*
+ * decode_attn.h -- C ABI of the MI355X (gfx950) decode-attention library.
+ *
+ * Single-query decode attention over a KV cache for MHA, GQA and MQA, and the
+ * per-step KV-cache append, as derived in "MoA-Structured Decode Attention:
+ * DNF Derivation, KV-Cache Accumulation, GQA/MQA, and OpenACC Kernel"
+ * (Mullin and Hains, 2026).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Every array argument is a DEVICE pointer (memory of the current
+ * HIP device) to contiguous row-major data, owned by the caller.  The library
+ * allocates nothing and keeps no pointer after a call returns.  Layouts are the
+ * row-major offsets of the paper's ONF section (element <l,j> of an <n,d_k>
+ * slab at l*d_k + j), lifted over batch and heads:
+ *     q     float [B][h_q][d_k]        query vector of every query head
+ *     K     float [B][h_kv][n_max][d_k] key cache, one slab per KV head
+ *     V     float [B][h_kv][n_max][d_v] value cache
+ *     len   int32 [B]                   valid rows per sequence (device)
+ *     out   float [B][h_q][d_v]         attention output
+ *     k_new float [B][h_kv][d_k], v_new float [B][h_kv][d_v]  rows to append
+ * n_max is the capacity (row stride of a slab).  Rows at or beyond len[b] may
+ * hold anything, NaN included: they are never read.
+ *
+ * Head map.  Query head h uses KV head floor(h*h_kv/h_q) (the psi-selection
+ * of eq. (10); h_kv must divide h_q), so the G = h_q/h_kv query heads of a
+ * group share one KV slab, which the decode reads from HBM once per group.
+ *
+ * Execution.  Calls only validate their arguments on the host and enqueue
+ * kernels on `stream` (a hipStream_t; NULL = the null stream); they return
+ * before the work runs.  Results are valid once the stream has reached that
+ * point.  Work enqueued on one stream runs in order, so an append followed by
+ * a decode on the same stream sees the appended row; `len` never needs to
+ * visit the host.
+ *
+ * Errors.  Every argument is checked before anything is enqueued; on a non-OK
+ * status nothing was enqueued and no memory was touched.  DA_ERR_HIP reports
+ * a launch failure from the HIP runtime.  No C++ exception crosses the ABI.
+ *
+ * Precision.  fp32 storage and arithmetic (the paper's 4-byte traffic model),
+ * products accumulated in fp32 by the matrix cores, exponentials by the
+ * hardware base-2 exponential.  Results agree with an exact evaluation within
+ * 1e-5 absolute for N(0,1) inputs; the append is a bit-exact copy.
+ */
+#ifndef DECODE_ATTN_H
+#define DECODE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum da_status {
+    DA_OK = 0,
+    DA_ERR_NULL = 1,        /* a required pointer is NULL                          */
+    DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q,
+                               or split_rows not a positive multiple of 64         */
+    DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128} (decode), or not a
+                               multiple of 4 (append)                              */
+    DA_ERR_ALIGN = 4,       /* a float array not 16-byte aligned, len not 4-byte   */
+    DA_ERR_SCALE = 5,       /* scale is NaN or infinite                            */
+    DA_ERR_WORKSPACE = 6,   /* workspace NULL or smaller than required             */
+    DA_ERR_HIP = 7          /* the HIP runtime reported an error at launch         */
+} da_status;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *da_status_string(int status);
+
+/*
+ * Rows of the KV cache one split partial covers (a positive multiple of 64)
+ * that the library picks for these shapes when split_rows is 0 below.
+ * Returns 0 if the shapes are invalid.
+ */
+int da_decode_split_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
+
+/*
+ * Bytes of device workspace da_decode_attn / da_decode_partial /
+ * da_decode_merge need for these shapes and split size (0 = the library's
+ * choice).  The workspace holds, per (b, query head, split), the running
+ * maximum, the running sum and the unnormalised weighted sum of the split's
+ * rows.  Returns 0 if the shapes are invalid.
+ */
+size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
+                                 int d_v, int split_rows);
+
+/*
+ * Decode attention, eqs. (1)-(3) (Algorithm 1) for every batch b and query
+ * head h, with the psi-selection head map of eq. (10):
+ *     s[l]  = scale * sum_j q[b,h,j] * K[b,g,l,j],   g = floor(h*h_kv/h_q),
+ *             for l < n_b = min(max(len[b], 0), n_max)
+ *     a     = softmax(s)                (max-subtracted, eq. (2))
+ *     out[b,h,d] = sum_l a[l] * V[b,g,l,d]
+ * n_b = 0 gives out[b,h,:] = 0.  `scale` is applied once to the dot product
+ * (the caller passes 1/sqrt(d_k) for standard attention).
+ *
+ * The cache rows are cut into splits of split_rows rows (0 = the library's
+ * choice); each split's softmax statistics and weighted sum are computed in
+ * one pass over its rows and the splits are then combined exactly (a
+ * regrouping of eqs. (2)-(3) over disjoint row sets).  Equivalent to
+ * da_decode_partial followed by da_decode_merge.
+ *
+ * Supported: d_k, d_v in {64, 128}; any B, h_q, h_kv >= 1 with h_kv | h_q.
+ * workspace: device memory of at least da_decode_workspace_bytes(...) bytes,
+ * 16-byte aligned; its contents on entry do not matter.  out must not overlap
+ * the inputs.
+ */
+da_status da_decode_attn(const float *q, const float *K, const float *V,
+                         const int32_t *len, float scale, float *out, int B,
+                         int h_q, int h_kv, int n_max, int d_k, int d_v,
+                         int split_rows, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
+/*
+ * First half of da_decode_attn: for every (b, KV head, split) the scores of
+ * all G query heads of the group over the split's rows, their maximum, the
+ * sum of exponentials relative to it and the unnormalised weighted sum of V
+ * rows, written to the workspace.  Splits starting at or beyond n_b are left
+ * untouched.  Arguments as for da_decode_attn (no `out`).
+ */
+da_status da_decode_partial(const float *q, const float *K, const float *V,
+                            const int32_t *len, float scale, int B, int h_q,
+                            int h_kv, int n_max, int d_k, int d_v,
+                            int split_rows, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/*
+ * Second half of da_decode_attn: combines the split partials of every
+ * (b, query head) into out[b,h,:] (global maximum, rescaled sums, one
+ * division).  split_rows and the shapes must be those of the
+ * da_decode_partial call that filled the workspace.
+ */
+da_status da_decode_merge(const int32_t *len, float *out, int B, int h_q,
+                          int h_kv, int n_max, int d_k, int d_v,
+                          int split_rows, const void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/*
+ * KV-cache append, eqs. (6)-(7) (K_{t+1} = K_t # k_t, V_{t+1} = V_t # v_t,
+ * Proposition 2): for every b with 0 <= t = len[b] < n_max and every KV head
+ * g, copies k_new[b,g,:] to K[b,g,t,:] and v_new[b,g,:] to V[b,g,t,:] bit for
+ * bit, then sets len[b] = t + 1.  No other cache row is touched.  A sequence
+ * whose cache is full (len[b] >= n_max) or whose len[b] is negative is left
+ * unchanged, len included.
+ * Supported: d_k, d_v positive multiples of 4; 16-byte aligned float arrays.
+ */
+da_status da_kv_append(float *K, float *V, const float *k_new,
+                       const float *v_new, int32_t *len, int B, int h_kv,
+                       int n_max, int d_k, int d_v, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DECODE_ATTN_H */

@@ -1,0 +1,172 @@
+"""Thin ctypes binding of ``libdecode_attn.so`` (the C ABI of
+``include/decode_attn.h``) for torch tensors.
+
+Argument marshalling only: every step of the decode runs in the HIP kernels
+behind the C ABI.  There is no fallback: if the library is missing or a call
+returns an error status, a Python exception is raised.
+
+Tensors must be contiguous, on the current HIP device, float32 (int32 for
+``len``).  Calls are asynchronous on torch's current stream (or ``stream``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY_PATH = os.environ.get("DECODE_ATTN_LIB", os.path.join(_PKG, "libdecode_attn.so"))
+
+STATUS = {
+    0: "DA_OK", 1: "DA_ERR_NULL", 2: "DA_ERR_SHAPE", 3: "DA_ERR_UNSUPPORTED",
+    4: "DA_ERR_ALIGN", 5: "DA_ERR_SCALE", 6: "DA_ERR_WORKSPACE", 7: "DA_ERR_HIP",
+}
+
+# Every symbol the header declares, with its ctypes signature.
+_vp, _ci, _cf, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+SIGNATURES = {
+    "da_status_string": (ctypes.c_char_p, [_ci]),
+    "da_decode_split_rows": (_ci, [_ci] * 6),
+    "da_decode_workspace_bytes": (_sz, [_ci] * 7),
+    "da_decode_attn": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_partial": (_ci, [_vp, _vp, _vp, _vp, _cf] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
+}
+
+
+class DecodeAttnError(RuntimeError):
+    """A non-OK status from the library."""
+
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {_lib.da_status_string(status).decode()}")
+
+
+def _load():
+    if not os.path.exists(LIBRARY_PATH):
+        raise ImportError(
+            f"HIP library {LIBRARY_PATH} is not built; run __graft_entry__.build() "
+            "(there is no CPU fallback)")
+    lib = ctypes.CDLL(LIBRARY_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise DecodeAttnError(fn, status)
+
+
+def _dev(t: torch.Tensor, name: str, dtype) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise TypeError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def split_rows(B, h_q, h_kv, n_max, d_k, d_v) -> int:
+    """Rows per split the library picks for these shapes (0: invalid)."""
+    return int(_lib.da_decode_split_rows(B, h_q, h_kv, n_max, d_k, d_v))
+
+
+def workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows: int = 0) -> int:
+    """Workspace bytes a decode with these shapes and split size needs."""
+    return int(_lib.da_decode_workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows))
+
+
+def _shapes(q, K, V):
+    if q.dim() != 3 or K.dim() != 4 or V.dim() != 4:
+        raise ValueError("q must be [B,h_q,d_k], K [B,h_kv,n_max,d_k], V [B,h_kv,n_max,d_v]")
+    B, h_q, d_k = q.shape
+    Bk, h_kv, n_max, d_k2 = K.shape
+    Bv, h_kv2, n_max2, d_v = V.shape
+    if not (B == Bk == Bv and h_kv == h_kv2 and n_max == n_max2 and d_k == d_k2):
+        raise ValueError("inconsistent q/K/V shapes")
+    return B, h_q, h_kv, n_max, d_k, d_v
+
+
+def alloc_workspace(q, K, V, split_rows: int = 0) -> torch.Tensor:
+    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    n = workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows)
+    if n == 0:
+        _check("da_decode_workspace_bytes", 2)
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def _ws(ws):
+    if ws.dtype != torch.uint8 or not ws.is_cuda or not ws.is_contiguous():
+        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+    return ws.data_ptr(), ws.numel()
+
+
+def decode_attn(q, K, V, lens, scale: float, out=None, workspace=None,
+                split_rows: int = 0, stream=None) -> torch.Tensor:
+    """out[b,h,:] = softmax(scale * K[b,g] q[b,h]) V[b,g] over len[b] rows."""
+    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    if out is None:
+        out = torch.empty((B, h_q, d_v), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(q, K, V, split_rows)
+    wp, wn = _ws(workspace)
+    _check("da_decode_attn", _lib.da_decode_attn(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
+        d_v, int(split_rows), wp, wn, _stream(stream)))
+    return out
+
+
+def decode_partial(q, K, V, lens, scale: float, workspace, split_rows: int = 0,
+                   stream=None) -> None:
+    """Split partials of the decode into ``workspace``."""
+    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    wp, wn = _ws(workspace)
+    _check("da_decode_partial", _lib.da_decode_partial(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), B, h_q, h_kv, n_max, d_k, d_v, int(split_rows), wp, wn,
+        _stream(stream)))
+
+
+def decode_merge(lens, out, workspace, B, h_q, h_kv, n_max, d_k, d_v,
+                 split_rows: int = 0, stream=None) -> torch.Tensor:
+    """Combine the split partials in ``workspace`` into ``out``."""
+    wp, wn = _ws(workspace)
+    _check("da_decode_merge", _lib.da_decode_merge(
+        _dev(lens, "len", torch.int32), _dev(out, "out", torch.float32), B, h_q,
+        h_kv, n_max, d_k, d_v, int(split_rows), wp, wn, _stream(stream)))
+    return out
+
+
+def kv_append(K, V, k_new, v_new, lens, stream=None) -> None:
+    """Write k_new/v_new at row len[b] of every KV head, then len[b] += 1."""
+    if K.dim() != 4 or V.dim() != 4:
+        raise ValueError("K and V must be [B,h_kv,n_max,d]")
+    B, h_kv, n_max, d_k = K.shape
+    d_v = V.shape[3]
+    if tuple(V.shape[:3]) != (B, h_kv, n_max):
+        raise ValueError("K and V disagree in [B,h_kv,n_max]")
+    if tuple(k_new.shape) != (B, h_kv, d_k) or tuple(v_new.shape) != (B, h_kv, d_v):
+        raise ValueError("k_new must be [B,h_kv,d_k] and v_new [B,h_kv,d_v]")
+    _check("da_kv_append", _lib.da_kv_append(
+        _dev(K, "K", torch.float32), _dev(V, "V", torch.float32),
+        _dev(k_new, "k_new", torch.float32), _dev(v_new, "v_new", torch.float32),
+        _dev(lens, "len", torch.int32), B, h_kv, n_max, d_k, d_v, _stream(stream)))

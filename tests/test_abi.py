@@ -1,0 +1,133 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and its host-side validation rejects bad arguments before anything
+is enqueued (these calls never reach the GPU, so they run without one)."""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "decode_attn.h")
+
+binding = pytest.importorskip("paper_2607_19456_amd.binding",
+                              reason="HIP library not built")
+lib = binding._lib
+
+FAKE = 0x10000   # a 16-byte aligned, never dereferenced address
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"\b(da_[a-z_]+)\s*\(", text))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert names == set(binding.SIGNATURES), names ^ set(binding.SIGNATURES)
+    for n in names:
+        assert hasattr(lib, n)
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIBRARY_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (da_[a-z_]+)\b", out))
+    assert names <= exported
+
+
+def test_status_strings():
+    for code, name in binding.STATUS.items():
+        assert lib.da_status_string(code).decode().startswith(name)
+    assert b"unknown" in lib.da_status_string(99)
+
+
+def test_split_rows_and_workspace_sizes():
+    for args in [(1, 1, 1, 128, 64, 64), (8, 32, 32, 4112, 128, 128),
+                 (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
+                 (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]:
+        B, h_q, h_kv, n_max, d_k, d_v = args
+        s = binding.split_rows(*args)
+        assert s >= 64 and s % 64 == 0
+        P = -(-n_max // s)
+        slots = B * h_q * P
+        ml = -(-slots * 8 // 256) * 256
+        assert binding.workspace_bytes(*args) == ml + slots * d_v * 4
+        assert binding.workspace_bytes(*args, 64) >= binding.workspace_bytes(*args)
+    assert binding.split_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
+    assert binding.workspace_bytes(1, 1, 1, 10, 96, 64) == 0  # unsupported d_k
+    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 100) == 0  # split not a multiple of 64
+
+
+def _decode(**kw):
+    a = dict(q=FAKE, K=FAKE, V=FAKE, len=FAKE, scale=0.125, out=FAKE, B=1, h_q=1,
+             h_kv=1, n_max=128, d_k=64, d_v=64, split=0, ws=FAKE, wsn=1 << 30,
+             stream=None)
+    a.update(kw)
+    return lib.da_decode_attn(a["q"], a["K"], a["V"], a["len"], a["scale"], a["out"],
+                              a["B"], a["h_q"], a["h_kv"], a["n_max"], a["d_k"],
+                              a["d_v"], a["split"], a["ws"], a["wsn"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), 1), (dict(K=None), 1), (dict(V=None), 1), (dict(len=None), 1),
+    (dict(out=None), 1),
+    (dict(B=0), 2), (dict(h_q=0), 2), (dict(h_kv=0), 2), (dict(n_max=0), 2),
+    (dict(h_q=3, h_kv=2), 2), (dict(B=70000), 2), (dict(split=100), 2),
+    (dict(split=32), 2),
+    (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=256), 3),
+    (dict(q=FAKE + 4), 4), (dict(K=FAKE + 8), 4), (dict(out=FAKE + 4), 4),
+    (dict(len=FAKE + 2), 4),
+    (dict(scale=float("nan")), 5), (dict(scale=float("inf")), 5),
+    (dict(ws=None), 6), (dict(wsn=16), 6),
+    (dict(ws=FAKE + 4), 4),
+])
+def test_decode_validation(kw, status):
+    assert _decode(**kw) == status
+
+
+def test_partial_and_merge_validation():
+    p = lib.da_decode_partial(None, FAKE, FAKE, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+                              FAKE, 1 << 20, None)
+    assert p == 1
+    p = lib.da_decode_partial(FAKE, FAKE, FAKE, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+                              FAKE, 8, None)
+    assert p == 6
+    m = lib.da_decode_merge(FAKE, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
+    assert m == 1
+    m = lib.da_decode_merge(FAKE, FAKE, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None)
+    assert m == 2
+    m = lib.da_decode_merge(FAKE, FAKE, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None)
+    assert m == 6
+
+
+@pytest.mark.parametrize("args,status", [
+    ((None, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64), 1),
+    ((FAKE, FAKE, FAKE, FAKE, None, 1, 1, 8, 64, 64), 1),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, 0, 1, 8, 64, 64), 2),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 64, 64), 2),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 62, 64), 3),
+    ((FAKE, FAKE + 4, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64), 4),
+    ((FAKE, FAKE, FAKE, FAKE + 8, FAKE, 1, 1, 8, 64, 64), 4),
+])
+def test_append_validation(args, status):
+    assert lib.da_kv_append(*args, None) == status
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    env = dict(os.environ, DECODE_ATTN_LIB=str(tmp_path / "missing.so"))
+    code = ("import paper_2607_19456_amd as p\n"
+            "try:\n    p.decode_attn\nexcept ImportError as e:\n    print('IMPORTERROR', e)\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=120)
+    assert "IMPORTERROR" in r.stdout and "no CPU fallback" in r.stdout
+
+
+def test_product_path_does_not_reference_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2607_19456_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".c", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "liboracle" not in text, f

@@ -1,0 +1,244 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Decode: max-abs-err <= 1e-5 against the fp64 oracle on the same seeded
+N(0,1) inputs, with every cache row at or beyond len[b] poisoned with NaN.
+Append: bit-exact against the oracle's host mirror.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_19456_amd import binding, workloads
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def dev(a, device):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def run_decode(inp, device, q=None, lens=None, split_rows=0, K=None, V=None):
+    s = inp.shape
+    q = inp.q if q is None else q
+    lens = inp.lens if lens is None else lens
+    dK = dev(inp.K, device) if K is None else K
+    dV = dev(inp.V, device) if V is None else V
+    dq, dl = dev(q, device), dev(lens, device)
+    ws = binding.alloc_workspace(dq, dK, dV, split_rows)
+    ws.view(torch.uint8).fill_(0xFF)         # NaN-poison the partials
+    out = binding.decode_attn(dq, dK, dV, dl, float(s.scale32()), workspace=ws,
+                              split_rows=split_rows)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64)
+
+
+def check(got, ref, what):
+    assert got.shape == ref.shape
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    say(f"  {what}: max-abs-err {err:.3e}")
+    assert err <= TOL, f"{what}: max-abs-err {err:.3e} > {TOL}"
+
+
+# --- decode on small shapes: several tiles, ragged tails, every group size --
+
+SMALL = [
+    # name, B, h_q, h_kv, d_k, d_v, n_max, lens
+    ("mha_d64", 2, 4, 4, 64, 64, 300, [300, 1]),
+    ("mha_d128_tail", 3, 2, 2, 128, 128, 1000, [17, 999, 64]),
+    ("gqa4", 2, 16, 4, 128, 128, 777, [777, 130]),
+    ("gqa8", 2, 16, 2, 128, 128, 2050, [2050, 1025]),
+    ("gqa16", 1, 16, 1, 128, 128, 333, [333]),
+    ("gqa20_twoblocks", 2, 40, 2, 128, 128, 200, [200, 63]),
+    ("mqa32", 2, 32, 1, 128, 128, 513, [513, 16]),
+    ("gqa64_headgroups", 1, 64, 1, 128, 128, 150, [150]),
+    ("dk64_dv128", 2, 8, 2, 64, 128, 400, [400, 65]),
+    ("dk128_dv64", 2, 8, 4, 128, 64, 400, [15, 400]),
+    ("g3_odd", 2, 9, 3, 64, 64, 97, [97, 2]),
+    ("empty_and_full", 3, 8, 8, 128, 128, 70, [0, 70, 1]),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("split_rows", [0, 64, 192])
+def test_decode_small_shapes(cuda_device, case, split_rows):
+    name, B, h_q, h_kv, d_k, d_v, n_max, lens = case
+    shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v,
+                             n_max=n_max)
+    inp = workloads.make(shape, seed=zlib.crc32(name.encode()) % 1000, lens=np.array(lens, np.int32))
+    say(f"decode {name} split_rows={split_rows} lens={lens}")
+    got = run_decode(inp, cuda_device, split_rows=split_rows)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, name)
+    for b, n in enumerate(lens):
+        if n == 0:
+            assert np.array_equal(got[b], np.zeros_like(got[b]))
+
+
+def test_split_count_invariance(cuda_device):
+    shape = workloads.custom("split", B=2, h_q=8, h_kv=2, d_k=128, d_v=128, n_max=4096)
+    inp = workloads.make(shape, seed=5, lens=np.array([4096, 3000], np.int32))
+    outs = [run_decode(inp, cuda_device, split_rows=s) for s in (64, 512, 4096, 0)]
+    for o in outs[1:]:
+        assert np.max(np.abs(o - outs[0])) <= 1e-6
+
+
+def test_len_beyond_capacity_is_clamped(cuda_device):
+    shape = workloads.custom("clamp", B=2, h_q=4, h_kv=2, d_k=64, d_v=64, n_max=100)
+    inp = workloads.make(shape, seed=6, lens=np.array([100, 100], np.int32))
+    got = run_decode(inp, cuda_device, lens=np.array([100000, -5], np.int32))
+    ref = oracle.decode(inp.q, inp.K, inp.V, np.array([100, 0], np.int32), shape.scale32())
+    check(got, ref, "clamped len")
+
+
+def test_identical_keys_give_mean_of_v(cuda_device):
+    shape = workloads.custom("ident", B=1, h_q=8, h_kv=1, d_k=128, d_v=128, n_max=1000)
+    inp = workloads.make(shape, seed=7)
+    inp.K[:] = inp.K[:, :, :1]
+    got = run_decode(inp, cuda_device)
+    mean = inp.V[0, 0].astype(np.float64).mean(axis=0)
+    for h in range(8):
+        assert np.max(np.abs(got[0, h] - mean)) <= TOL
+
+
+def test_large_logits_stay_finite(cuda_device):
+    shape = workloads.custom("big", B=1, h_q=4, h_kv=1, d_k=128, d_v=128, n_max=500,
+                             scale=1.0)
+    inp = workloads.make(shape, seed=8)
+    inp.q *= 4                       # scores of several hundred
+    got = run_decode(inp, cuda_device)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, "large logits")
+
+
+def test_decode_partial_then_merge_equals_decode(cuda_device):
+    shape = workloads.custom("pm", B=2, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=900)
+    inp = workloads.make(shape, seed=9, lens=np.array([900, 450], np.int32))
+    dq, dK, dV, dl = (dev(a, cuda_device) for a in (inp.q, inp.K, inp.V, inp.lens))
+    ws = binding.alloc_workspace(dq, dK, dV)
+    out = torch.empty((2, 16, 128), device=cuda_device)
+    binding.decode_partial(dq, dK, dV, dl, float(shape.scale32()), ws)
+    binding.decode_merge(dl, out, ws, 2, 16, 2, 900, 128, 128)
+    torch.cuda.synchronize()
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(out.cpu().numpy().astype(np.float64), ref, "partial+merge")
+
+
+def test_validation_errors_raise(cuda_device):
+    shape = workloads.custom("err", B=1, h_q=2, h_kv=1, d_k=64, d_v=64, n_max=64)
+    inp = workloads.make(shape, seed=1)
+    dq, dK, dV, dl = (dev(a, cuda_device) for a in (inp.q, inp.K, inp.V, inp.lens))
+    small = torch.empty(8, dtype=torch.uint8, device=cuda_device)
+    with pytest.raises(binding.DecodeAttnError, match="WORKSPACE"):
+        binding.decode_attn(dq, dK, dV, dl, 0.1, workspace=small)
+    with pytest.raises(binding.DecodeAttnError, match="SCALE"):
+        binding.decode_attn(dq, dK, dV, dl, float("nan"))
+
+
+# --- append: bit-exact --------------------------------------------------------
+
+@pytest.mark.parametrize("d_k,d_v", [(128, 128), (64, 128), (4, 12)])
+def test_append_bit_exact(cuda_device, d_k, d_v):
+    B, h_kv, n_max = 3, 5, 9
+    rng = np.random.default_rng([d_k, d_v])
+    K = rng.standard_normal((B, h_kv, n_max, d_k)).astype(np.float32)
+    V = rng.standard_normal((B, h_kv, n_max, d_v)).astype(np.float32)
+    lens = np.array([0, 4, 8], np.int32)
+    dK, dV, dl = dev(K, cuda_device), dev(V, cuda_device), dev(lens, cuda_device)
+    for step in range(3):   # the third sequence fills up after one append
+        kn = rng.standard_normal((B, h_kv, d_k)).astype(np.float32)
+        vn = rng.standard_normal((B, h_kv, d_v)).astype(np.float32)
+        # odd bit patterns must survive: NaN payloads, -0, denormals, inf
+        kn.view(np.uint32)[0, 0, :4] = [0x7FC01234, 0xFFA00001, 0x80000000, 0x00000001]
+        vn.view(np.uint32)[1, 2, :2] = [0x7F800000, 0x7F812345]
+        say(f"append d_k={d_k} d_v={d_v} step={step}")
+        binding.kv_append(dK, dV, dev(kn, cuda_device), dev(vn, cuda_device), dl)
+        oracle.append(K, V, kn, vn, lens)
+        torch.cuda.synchronize()
+        assert np.array_equal(dl.cpu().numpy(), lens)
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), K.view(np.uint32))
+        assert np.array_equal(dV.cpu().numpy().view(np.uint32), V.view(np.uint32))
+    assert lens.tolist() == [3, 7, 9]
+
+
+def test_append_with_negative_len_is_a_no_op(cuda_device):
+    K = torch.zeros((2, 1, 4, 4), device=cuda_device)
+    V = torch.zeros((2, 1, 4, 4), device=cuda_device)
+    lens = torch.tensor([-1, 4], dtype=torch.int32, device=cuda_device)
+    one = torch.ones((2, 1, 4), device=cuda_device)
+    binding.kv_append(K, V, one, one, lens)
+    torch.cuda.synchronize()
+    assert lens.tolist() == [-1, 4] and not K.any() and not V.any()
+
+
+# --- the five workloads -------------------------------------------------------
+
+def _sample_heads(B, h_q, count, seed):
+    rng = np.random.default_rng(seed)
+    mask = np.zeros((B, h_q), bool)
+    for b in range(B):
+        mask[b, rng.choice(h_q, size=min(count, h_q), replace=False)] = True
+        mask[b, 0] = mask[b, h_q - 1] = True
+    return mask
+
+
+@pytest.mark.parametrize("name", ["c1", "c3", "c4"])
+def test_single_step_workloads(cuda_device, name):
+    shape = workloads.get(name)
+    say(f"workload {shape.name}: generating inputs")
+    inp = workloads.make(shape, seed=0)
+    say(f"workload {shape.name}: decode")
+    got = run_decode(inp, cuda_device)
+    heads = None if name in ("c1", "c3") else _sample_heads(shape.B, shape.h_q, 6, 1)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32(), heads=heads)
+    sel = np.ones((shape.B, shape.h_q), bool) if heads is None else heads
+    check(got[sel], ref[sel], shape.name)
+
+
+@pytest.mark.parametrize("name,check_steps,heads_per_b",
+                         [("c2", None, 3), ("c5", (0, 1, 31, 62, 63), 2)])
+def test_multi_step_workloads(cuda_device, name, check_steps, heads_per_b):
+    """Append then decode, step after step, with len kept on the device; the
+    host mirror replays every append and the oracle checks sampled heads."""
+    shape = workloads.get(name)
+    say(f"workload {shape.name}: generating inputs")
+    inp = workloads.make(shape, seed=0)
+    dK, dV = dev(inp.K, cuda_device), dev(inp.V, cuda_device)
+    dl = dev(inp.lens, cuda_device)
+    hK, hV, hl = inp.K, inp.V, inp.lens.copy()
+    dq0 = dev(inp.q_step[0], cuda_device)
+    ws = binding.alloc_workspace(dq0, dK, dV)
+    out = torch.empty((shape.B, shape.h_q, shape.d_v), device=cuda_device)
+    steps = range(shape.steps) if check_steps is None else check_steps
+    for t in range(shape.steps):
+        binding.kv_append(dK, dV, dev(inp.k_new[t], cuda_device),
+                          dev(inp.v_new[t], cuda_device), dl)
+        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+        dq = dev(inp.q_step[t], cuda_device)
+        binding.decode_attn(dq, dK, dV, dl, float(shape.scale32()), out=out, workspace=ws)
+        if t in steps:
+            torch.cuda.synchronize()
+            say(f"workload {shape.name}: step {t} check")
+            assert np.array_equal(dl.cpu().numpy(), hl)
+            heads = _sample_heads(shape.B, shape.h_q, heads_per_b, t)
+            ref = oracle.decode(inp.q_step[t], hK, hV, hl, shape.scale32(), heads=heads)
+            got = out.cpu().numpy().astype(np.float64)
+            check(got[heads], ref[heads], f"{shape.name} step {t}")
+            # the appended rows themselves, bit for bit
+            for b in range(shape.B):
+                r = int(hl[b]) - 1
+                assert np.array_equal(dK[b, :, r].cpu().numpy().view(np.uint32),
+                                      hK[b, :, r].view(np.uint32))
+                assert np.array_equal(dV[b, :, r].cpu().numpy().view(np.uint32),
+                                      hV[b, :, r].view(np.uint32))
+    torch.cuda.synchronize()
+    assert np.array_equal(dl.cpu().numpy(), hl)
