@@ -1,0 +1,305 @@
+#!/usr/bin/env python3
+"""Benchmark of the decode-attention hot path on one MI355X.
+
+One step = one pass of the whole path over one batch: KV append (every KV
+head of every sequence gets one new row) followed by decode attention of
+every query head (split partials, then the merge).  The default workload is
+the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
+len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
+
+Prints ONE JSON line:
+  value        algorithmic HBM bytes of the step (paper's traffic model:
+               K/V rows read once per KV head over len_b rows, q read and
+               output written once per query head, the appended rows) divided
+               by the measured time per step, in GB/s; inputs are resident in
+               HBM before the timed region starts.
+  roofline     the dominant kernel (decode_partial_kernel): its algorithmic
+               bytes per launch over its average launch duration, measured with
+               HIP events on the stream it runs on, against the 8 TB/s HBM peak;
+               `traffic` = HBM bytes per launch from rocprofv3 FETCH_SIZE and
+               WRITE_SIZE counters (profiles/decode_partial_counters.json),
+               null when the kernel source changed since they were taken.
+  cpu_baseline the CPU oracle (plain fp64 loops, OpenMP over heads) timed on
+               this host on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "achieved HBM GB/s and µs per decode step (fp32 GQA), % of HBM roofline"
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_19456_amd", "csrc", "decode_attn.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "decode_partial_counters.json")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per decode_partial launch from the committed counter runs,
+    or None when they are absent, for another workload, or stale."""
+    try:
+        with open(COUNTERS) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("kernel_source_sha256") != kernel_source_hash() or c.get("workload") != workload:
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def host_cores() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(inp, budget_s: float, step_bytes):
+    """Time the oracle (append + decode of every head, step after step) on
+    this host until about budget_s seconds of work are done."""
+    import numpy as np
+
+    import oracle
+
+    s = inp.shape
+    threads = host_cores()
+    hK, hV, hl = inp.K, inp.V, inp.lens.copy()
+    done, elapsed, nbytes = 0, 0.0, 0
+    steps = max(1, s.steps)
+    while True:
+        t = done % steps
+        t0 = time.perf_counter()
+        if s.steps:
+            oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+            q = inp.q_step[t]
+        else:
+            q = inp.q
+        oracle.decode(q, hK, hV, hl, s.scale32(), threads=threads)
+        elapsed += time.perf_counter() - t0
+        nbytes += step_bytes(hl, bool(s.steps))
+        done += 1
+        log(f"cpu_baseline: oracle step {done} ({elapsed:.1f} s)")
+        if elapsed >= budget_s or (s.steps and done >= s.steps):
+            break
+    return {
+        "value": nbytes / elapsed / 1e9,
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"{done} full step(s) (append + decode of all {s.B * s.h_q} query "
+                   f"heads) of the same workload, {elapsed:.2f} s, fp64 oracle, "
+                   f"{threads} OpenMP threads"),
+        "seconds_per_step": elapsed / done,
+        "cpu_model": _cpu_model(),
+    }
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5")
+    ap.add_argument("--split-rows", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (for counter scaling)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not "
+              "supported (the decode would shard by KV head with no exchange, "
+              "see the design notes)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_19456_amd import binding, traffic, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        a = torch.empty(n // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
+        return 0
+
+    shape = workloads.get(args.workload)
+    s = shape
+    log(f"workload {s.name}: drawing inputs")
+    t0 = time.perf_counter()
+    inp = workloads.make(shape, seed=0, pad=0.0)
+    log(f"inputs drawn in {time.perf_counter() - t0:.1f} s; copying to HBM")
+
+    dK = torch.from_numpy(inp.K).to(dev)
+    dV = torch.from_numpy(inp.V).to(dev)
+    lens0 = torch.from_numpy(inp.lens).to(dev)
+    dl = lens0.clone()
+    nsteps_in = max(1, s.steps)
+    if s.steps:
+        dkn = torch.from_numpy(inp.k_new).to(dev)
+        dvn = torch.from_numpy(inp.v_new).to(dev)
+        dq = torch.from_numpy(inp.q_step).to(dev)
+    else:
+        dq = torch.from_numpy(inp.q[None]).to(dev)
+    out = torch.empty((s.B, s.h_q, s.d_v), dtype=torch.float32, device=dev)
+    split = args.split_rows or binding.split_rows(s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v)
+    ws = binding.alloc_workspace(dq[0], dK, dV, split)
+    scale = float(s.scale32())
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(i, ev_a=None, ev_b=None):
+        t = i % nsteps_in
+        if s.steps:
+            if t == 0 and i > 0:
+                dl.copy_(lens0)          # a new pass over the 64-step sequence
+            binding.kv_append(dK, dV, dkn[t], dvn[t], dl, stream=stream)
+        if ev_a is not None:
+            ev_a.record(stream)
+        binding.decode_partial(dq[t], dK, dV, dl, scale, ws, split, stream=stream)
+        if ev_b is not None:
+            ev_b.record(stream)
+        binding.decode_merge(dl, out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
+                             split, stream=stream)
+
+    log(f"warmup {args.warmup} step(s), split_rows={split}")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    dl.copy_(lens0)
+    torch.cuda.synchronize()
+
+    # Host-side mirror of the lengths each timed step decodes over.
+    lens_host = inp.lens.astype(np.int64)
+    step_lens = []
+    for i in range(args.steps):
+        t = i % nsteps_in
+        if s.steps:
+            if t == 0 and i > 0:
+                lens_host = inp.lens.astype(np.int64)
+            lens_host = np.minimum(lens_host + 1, s.n_max)
+        step_lens.append(lens_host.copy())
+
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} step(s)")
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(i, ev_a[i], ev_b[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    partial_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
+
+    def step_bytes(lens, with_append=True):
+        b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v)
+        if with_append:
+            b += traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v)
+        return b
+
+    alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
+    partial_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v)
+                     for l in step_lens]
+    ms_per_step = total_ms / args.steps
+    value = alg_bytes / (total_ms * 1e-3) / 1e9
+    part_avg_ms = sum(partial_ms) / len(partial_ms)
+    achieved = (sum(partial_bytes) / len(partial_bytes)) / (part_avg_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": s.name,
+            "B": s.B, "h_q": s.h_q, "h_kv": s.h_kv, "d_k": s.d_k, "d_v": s.d_v,
+            "n_max": s.n_max,
+            "initial_len": [int(x) for x in inp.lens],
+            "steps_per_sequence": s.steps,
+            "split_rows": split,
+            "step": "kv_append + decode_partial + decode_merge" if s.steps
+                    else "decode_partial + decode_merge",
+        },
+        "us_per_step": round(ms_per_step * 1e3, 2),
+        "hbm_roofline_frac_step": round(value / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": int(alg_bytes / args.steps),
+        "host_wall_s": round(wall, 4),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode_partial_kernel",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": counter_traffic(s.name),
+            "avg_launch_us": round(part_avg_ms * 1e3, 2),
+            "algorithmic_bytes_per_launch": int(sum(partial_bytes) / len(partial_bytes)),
+        },
+    }
+    log(f"{ms_per_step * 1e3:.1f} us/step, {value:.0f} GB/s; partial "
+        f"{part_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
+
+    del dK, dV
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        log("cpu_baseline: timing the oracle on this host")
+        # the oracle replays the workload from its initial state
+        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, step_bytes)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
