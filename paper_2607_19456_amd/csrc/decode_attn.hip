@@ -137,24 +137,32 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T,
 // cores, online softmax update, weighted-sum update on the matrix cores.
 template <int DK, int DV, int NB>
 __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0, int last_row,
-                                             int k, const f4 (&qb)[NB][DK / 16],
+                                             int k, int lane,
+                                             const f4 (*__restrict__ sh_q)[DK / 16][kWave],
                                              float (&m_run)[NB], float (&l_run)[NB],
                                              f4 (&acc)[NB][DV / 64][4]) {
+  // q is re-read from LDS for every tile rather than pinned in 32 VGPRs per
+  // column block: the empty asm keeps the compiler from hoisting those reads
+  // out of the tile loop, which would cost a second wave per SIMD.
+  asm volatile("" ::: "memory");
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    f4 qb[DK / 16];
+#pragma unroll
+    for (int t = 0; t < DK / 16; ++t) qb[t] = sh_q[nb][t][lane];
     // Step I: s[row 4k+r][head i] for the tile's 16 rows (two independent
     // accumulation chains over the d_k/4 steps, added at the end).
     f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < DK / 16; t += 2) {
-      s0 = mfma_16x16x4(T.k[t].x, qb[nb][t].x, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].x, qb[nb][t + 1].x, s1);
-      s0 = mfma_16x16x4(T.k[t].y, qb[nb][t].y, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].y, qb[nb][t + 1].y, s1);
-      s0 = mfma_16x16x4(T.k[t].z, qb[nb][t].z, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].z, qb[nb][t + 1].z, s1);
-      s0 = mfma_16x16x4(T.k[t].w, qb[nb][t].w, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].w, qb[nb][t + 1].w, s1);
+      s0 = mfma_16x16x4(T.k[t].x, qb[t].x, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].x, qb[t + 1].x, s1);
+      s0 = mfma_16x16x4(T.k[t].y, qb[t].y, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].y, qb[t + 1].y, s1);
+      s0 = mfma_16x16x4(T.k[t].z, qb[t].z, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].z, qb[t + 1].z, s1);
+      s0 = mfma_16x16x4(T.k[t].w, qb[t].w, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].w, qb[t + 1].w, s1);
     }
     f4 s = s0 + s1;
     // Rows past the split's end take no weight.
@@ -223,21 +231,21 @@ __global__ __launch_bounds__(kThreads) void decode_partial_kernel(
   const float* __restrict__ Ks = K + slab * n_max * DK;
   const float* __restrict__ Vs = V + slab * n_max * DV;
 
-  // B operand of the score product: lane (k, i) holds q of head i of each
-  // column block at dims 16t+4k..+3, scaled into base-2 units.
-  f4 qb[NB][DK / 16];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int hl = nb * kHeadsPerBlock + i;
-    if (hl < h_count) {
-      const float* qrow = q + ((int64_t)b * h_q + h_first + hl) * DK;
-#pragma unroll
-      for (int t = 0; t < DK / 16; ++t) qb[nb][t] = load4(qrow + 16 * t + 4 * k) * qscale;
-    } else {
-#pragma unroll
-      for (int t = 0; t < DK / 16; ++t) qb[nb][t] = f4{0.f, 0.f, 0.f, 0.f};
-    }
+  // B operand of the score product, staged in LDS in register order: entry
+  // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
+  // base-2 units (zero for the padding heads of a partial column block).
+  __shared__ f4 sh_q[NB][DK / 16][kWave];
+  for (int e = threadIdx.x; e < NB * (DK / 16) * kWave; e += kThreads) {
+    const int ln = e % kWave;
+    const int t = (e / kWave) % (DK / 16);
+    const int nb = e / (kWave * (DK / 16));
+    const int hl = nb * kHeadsPerBlock + (ln & 15);
+    f4 v = f4{0.f, 0.f, 0.f, 0.f};
+    if (hl < h_count)
+      v = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4)) * qscale;
+    sh_q[nb][t][ln] = v;
   }
+  __syncthreads();
 
   // Running state per column block; lane (k, i) belongs to head i.
   float m_run[NB], l_run[NB];
@@ -261,12 +269,12 @@ __global__ __launch_bounds__(kThreads) void decode_partial_kernel(
   while (tile < n_tiles) {
     if (tile + kWaves < n_tiles)
       load_tile(tb, Ks, Vs, row_begin + (tile + kWaves) * kTileRows, last_row, i, k);
-    process_tile<DK, DV, NB>(ta, row_begin + tile * kTileRows, last_row, k, qb, m_run, l_run, acc);
+    process_tile<DK, DV, NB>(ta, row_begin + tile * kTileRows, last_row, k, lane, sh_q, m_run, l_run, acc);
     tile += kWaves;
     if (tile >= n_tiles) break;
     if (tile + kWaves < n_tiles)
       load_tile(ta, Ks, Vs, row_begin + (tile + kWaves) * kTileRows, last_row, i, k);
-    process_tile<DK, DV, NB>(tb, row_begin + tile * kTileRows, last_row, k, qb, m_run, l_run, acc);
+    process_tile<DK, DV, NB>(tb, row_begin + tile * kTileRows, last_row, k, lane, sh_q, m_run, l_run, acc);
     tile += kWaves;
   }
 
