@@ -3,7 +3,7 @@
 
 One step = one pass of the whole path over one batch: KV append (every KV
 head of every sequence gets one new row) followed by decode attention of
-every query head (split partials, then the merge).  The default workload is
+every query head (partials, then the merge).  The default workload is
 the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
 len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
 
@@ -129,7 +129,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5")
-    ap.add_argument("--split-rows", type=int, default=0)
+    ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle sample (0: skip)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -179,8 +179,8 @@ def main() -> int:
     else:
         dq = torch.from_numpy(inp.q[None]).to(dev)
     out = torch.empty((s.B, s.h_q, s.d_v), dtype=torch.float32, device=dev)
-    split = args.split_rows or binding.split_rows(s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v)
-    ws = binding.alloc_workspace(dq[0], dK, dV, split)
+    chunk = args.chunk_rows or binding.chunk_rows(s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v)
+    ws = binding.alloc_workspace(dq[0], dK, dV, chunk)
     scale = float(s.scale32())
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -193,13 +193,13 @@ def main() -> int:
             binding.kv_append(dK, dV, dkn[t], dvn[t], dl, stream=stream)
         if ev_a is not None:
             ev_a.record(stream)
-        binding.decode_partial(dq[t], dK, dV, dl, scale, ws, split, stream=stream)
+        binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=stream)
         if ev_b is not None:
             ev_b.record(stream)
-        binding.decode_merge(dl, out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
-                             split, stream=stream)
+        binding.decode_merge(out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
+                             chunk, stream=stream)
 
-    log(f"warmup {args.warmup} step(s), split_rows={split}")
+    log(f"warmup {args.warmup} step(s), chunk_rows={chunk}")
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -266,7 +266,7 @@ def main() -> int:
             "n_max": s.n_max,
             "initial_len": [int(x) for x in inp.lens],
             "steps_per_sequence": s.steps,
-            "split_rows": split,
+            "chunk_rows": chunk,
             "step": "kv_append + decode_partial + decode_merge" if s.steps
                     else "decode_partial + decode_merge",
         },

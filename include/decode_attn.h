@@ -56,7 +56,7 @@ typedef enum da_status {
     DA_OK = 0,
     DA_ERR_NULL = 1,        /* a required pointer is NULL                          */
     DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q,
-                               or split_rows not a positive multiple of 64         */
+                               or chunk_rows not a positive multiple of 192        */
     DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128} (decode), or not a
                                multiple of 4 (append)                              */
     DA_ERR_ALIGN = 4,       /* a float array not 16-byte aligned, len not 4-byte   */
@@ -69,21 +69,38 @@ typedef enum da_status {
 const char *da_status_string(int status);
 
 /*
- * Rows of the KV cache one split partial covers (a positive multiple of 64)
- * that the library picks for these shapes when split_rows is 0 below.
- * Returns 0 if the shapes are invalid.
+ * Workspace.  The decode keeps, per (b, query head), a few partial results
+ * (running maximum, running sum of exponentials, unnormalised weighted sum of
+ * V rows) plus three small counters per (b, KV head) that schedule the work.
+ * The counter region -- the first da_decode_workspace_counter_bytes() bytes
+ * -- must be zero before the first decode that uses the workspace (an
+ * all-zero workspace always qualifies); every completed decode (partial then
+ * merge) leaves it zero again, so a workspace can be reused call after call
+ * without clearing.  The rest of the workspace needs no initialisation.  One
+ * workspace serves one decode at a time: decodes that overlap in time (on
+ * different streams) need separate workspaces.
  */
-int da_decode_split_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
+
+/*
+ * Rows per work chunk the library picks for these shapes when chunk_rows is
+ * 0 below (a positive multiple of 192).  Returns 0 if the shapes are invalid.
+ */
+int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
 
 /*
  * Bytes of device workspace da_decode_attn / da_decode_partial /
- * da_decode_merge need for these shapes and split size (0 = the library's
- * choice).  The workspace holds, per (b, query head, split), the running
- * maximum, the running sum and the unnormalised weighted sum of the split's
- * rows.  Returns 0 if the shapes are invalid.
+ * da_decode_merge need for these shapes and chunk size (0 = the library's
+ * choice).  Returns 0 if the shapes or chunk_rows are invalid.
  */
 size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
-                                 int d_v, int split_rows);
+                                 int d_v, int chunk_rows);
+
+/*
+ * Leading bytes of that workspace that hold the scheduling counters (the part
+ * that must be zero before first use).  Returns 0 if the shapes are invalid.
+ */
+size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
+                                         int d_k, int d_v);
 
 /*
  * Decode attention, eqs. (1)-(3) (Algorithm 1) for every batch b and query
@@ -95,45 +112,48 @@ size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
  * n_b = 0 gives out[b,h,:] = 0.  `scale` is applied once to the dot product
  * (the caller passes 1/sqrt(d_k) for standard attention).
  *
- * The cache rows are cut into splits of split_rows rows (0 = the library's
- * choice); each split's softmax statistics and weighted sum are computed in
- * one pass over its rows and the splits are then combined exactly (a
- * regrouping of eqs. (2)-(3) over disjoint row sets).  Equivalent to
- * da_decode_partial followed by da_decode_merge.
+ * Each (b, KV head) slab's rows are cut into chunks of chunk_rows rows (0 =
+ * the library's choice) that a resident set of workgroups takes dynamically;
+ * a workgroup folds every chunk it takes from one slab into one running
+ * softmax state (the online form of eq. (2)) and leaves one partial per
+ * visit;
+ * the partials are then combined exactly (a regrouping of eqs. (2)-(3) over
+ * disjoint row sets).  The summation order therefore varies from call to call
+ * within fp32 rounding.  Equivalent to da_decode_partial followed by
+ * da_decode_merge.
  *
  * Supported: d_k, d_v in {64, 128}; any B, h_q, h_kv >= 1 with h_kv | h_q.
- * workspace: device memory of at least da_decode_workspace_bytes(...) bytes,
- * 16-byte aligned; its contents on entry do not matter.  out must not overlap
- * the inputs.
+ * workspace: see above; at least da_decode_workspace_bytes(...) bytes,
+ * 16-byte aligned.  out must not overlap the inputs.
  */
 da_status da_decode_attn(const float *q, const float *K, const float *V,
                          const int32_t *len, float scale, float *out, int B,
                          int h_q, int h_kv, int n_max, int d_k, int d_v,
-                         int split_rows, void *workspace,
+                         int chunk_rows, void *workspace,
                          size_t workspace_bytes, void *stream);
 
 /*
- * First half of da_decode_attn: for every (b, KV head, split) the scores of
- * all G query heads of the group over the split's rows, their maximum, the
- * sum of exponentials relative to it and the unnormalised weighted sum of V
- * rows, written to the workspace.  Splits starting at or beyond n_b are left
- * untouched.  Arguments as for da_decode_attn (no `out`).
+ * First half of da_decode_attn: scores of all G query heads of each group
+ * over the slab's rows (K and V rows read from HBM once per (b, KV head)),
+ * their running maxima, sums of exponentials and unnormalised weighted sums
+ * of V rows, written to the workspace as per-visit partials.  Must be
+ * followed by da_decode_merge on the same workspace (which also re-zeroes the
+ * counters).  Arguments as for da_decode_attn (no `out`).
  */
 da_status da_decode_partial(const float *q, const float *K, const float *V,
                             const int32_t *len, float scale, int B, int h_q,
                             int h_kv, int n_max, int d_k, int d_v,
-                            int split_rows, void *workspace,
+                            int chunk_rows, void *workspace,
                             size_t workspace_bytes, void *stream);
 
 /*
- * Second half of da_decode_attn: combines the split partials of every
- * (b, query head) into out[b,h,:] (global maximum, rescaled sums, one
- * division).  split_rows and the shapes must be those of the
- * da_decode_partial call that filled the workspace.
+ * Second half of da_decode_attn: combines the partials of every (b, query
+ * head) into out[b,h,:] (running maximum, rescaled sums, one division) and
+ * resets the workspace counters to zero.  chunk_rows and the shapes must be
+ * those of the da_decode_partial call that filled the workspace.
  */
-da_status da_decode_merge(const int32_t *len, float *out, int B, int h_q,
-                          int h_kv, int n_max, int d_k, int d_v,
-                          int split_rows, const void *workspace,
+da_status da_decode_merge(float *out, int B, int h_q, int h_kv, int n_max,
+                          int d_k, int d_v, int chunk_rows, void *workspace,
                           size_t workspace_bytes, void *stream);
 
 /*

@@ -12,7 +12,7 @@ from importlib import import_module
 
 _BINDING_NAMES = {
     "decode_attn", "decode_partial", "decode_merge", "kv_append",
-    "split_rows", "workspace_bytes", "alloc_workspace", "DecodeAttnError",
+    "chunk_rows", "workspace_bytes", "workspace_counter_bytes", "alloc_workspace", "DecodeAttnError",
     "LIBRARY_PATH",
 }
 

@@ -27,11 +27,12 @@ STATUS = {
 _vp, _ci, _cf, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 SIGNATURES = {
     "da_status_string": (ctypes.c_char_p, [_ci]),
-    "da_decode_split_rows": (_ci, [_ci] * 6),
+    "da_decode_chunk_rows": (_ci, [_ci] * 6),
     "da_decode_workspace_bytes": (_sz, [_ci] * 7),
+    "da_decode_workspace_counter_bytes": (_sz, [_ci] * 6),
     "da_decode_attn": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_decode_partial": (_ci, [_vp, _vp, _vp, _vp, _cf] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_merge": (_ci, [_vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
 }
 
@@ -82,14 +83,19 @@ def _stream(stream) -> int:
     return s.cuda_stream
 
 
-def split_rows(B, h_q, h_kv, n_max, d_k, d_v) -> int:
-    """Rows per split the library picks for these shapes (0: invalid)."""
-    return int(_lib.da_decode_split_rows(B, h_q, h_kv, n_max, d_k, d_v))
+def chunk_rows(B, h_q, h_kv, n_max, d_k, d_v) -> int:
+    """Rows per work chunk the library picks for these shapes (0: invalid)."""
+    return int(_lib.da_decode_chunk_rows(B, h_q, h_kv, n_max, d_k, d_v))
 
 
-def workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows: int = 0) -> int:
-    """Workspace bytes a decode with these shapes and split size needs."""
-    return int(_lib.da_decode_workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows))
+def workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows: int = 0) -> int:
+    """Workspace bytes a decode with these shapes and chunk size needs."""
+    return int(_lib.da_decode_workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows))
+
+
+def workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, d_v) -> int:
+    """Leading workspace bytes that must be zero before first use."""
+    return int(_lib.da_decode_workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, d_v))
 
 
 def _shapes(q, K, V):
@@ -103,12 +109,14 @@ def _shapes(q, K, V):
     return B, h_q, h_kv, n_max, d_k, d_v
 
 
-def alloc_workspace(q, K, V, split_rows: int = 0) -> torch.Tensor:
+def alloc_workspace(q, K, V, chunk_rows: int = 0) -> torch.Tensor:
+    """A zeroed workspace for decodes of these shapes (reusable across calls:
+    every completed decode leaves its counter region zero again)."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
-    n = workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, split_rows)
+    n = workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows)
     if n == 0:
         _check("da_decode_workspace_bytes", 2)
-    return torch.empty(n, dtype=torch.uint8, device=q.device)
+    return torch.zeros(n, dtype=torch.uint8, device=q.device)
 
 
 def _ws(ws):
@@ -118,41 +126,42 @@ def _ws(ws):
 
 
 def decode_attn(q, K, V, lens, scale: float, out=None, workspace=None,
-                split_rows: int = 0, stream=None) -> torch.Tensor:
+                chunk_rows: int = 0, stream=None) -> torch.Tensor:
     """out[b,h,:] = softmax(scale * K[b,g] q[b,h]) V[b,g] over len[b] rows."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     if out is None:
         out = torch.empty((B, h_q, d_v), dtype=torch.float32, device=q.device)
     if workspace is None:
-        workspace = alloc_workspace(q, K, V, split_rows)
+        workspace = alloc_workspace(q, K, V, chunk_rows)
     wp, wn = _ws(workspace)
     _check("da_decode_attn", _lib.da_decode_attn(
         _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
         _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
         float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
-        d_v, int(split_rows), wp, wn, _stream(stream)))
+        d_v, int(chunk_rows), wp, wn, _stream(stream)))
     return out
 
 
-def decode_partial(q, K, V, lens, scale: float, workspace, split_rows: int = 0,
+def decode_partial(q, K, V, lens, scale: float, workspace, chunk_rows: int = 0,
                    stream=None) -> None:
-    """Split partials of the decode into ``workspace``."""
+    """Partials of the decode into ``workspace`` (follow with decode_merge)."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     wp, wn = _ws(workspace)
     _check("da_decode_partial", _lib.da_decode_partial(
         _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
         _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
-        float(scale), B, h_q, h_kv, n_max, d_k, d_v, int(split_rows), wp, wn,
+        float(scale), B, h_q, h_kv, n_max, d_k, d_v, int(chunk_rows), wp, wn,
         _stream(stream)))
 
 
-def decode_merge(lens, out, workspace, B, h_q, h_kv, n_max, d_k, d_v,
-                 split_rows: int = 0, stream=None) -> torch.Tensor:
-    """Combine the split partials in ``workspace`` into ``out``."""
+def decode_merge(out, workspace, B, h_q, h_kv, n_max, d_k, d_v,
+                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
+    """Combine the partials in ``workspace`` into ``out`` (re-zeroes the
+    workspace counters)."""
     wp, wn = _ws(workspace)
     _check("da_decode_merge", _lib.da_decode_merge(
-        _dev(lens, "len", torch.int32), _dev(out, "out", torch.float32), B, h_q,
-        h_kv, n_max, d_k, d_v, int(split_rows), wp, wn, _stream(stream)))
+        _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k, d_v,
+        int(chunk_rows), wp, wn, _stream(stream)))
     return out
 
 

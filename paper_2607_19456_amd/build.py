@@ -23,6 +23,10 @@ FLAGS = [
     "-Wall", "-Wextra",
     # Keep the compiler from forming packed fp32 instructions.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # Leave single-lane atomics as they are: the optimizer's wave-wide
+    # rewrite reads the result at once, which stalls the load pipeline
+    # behind the work counter of the decode kernel.
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     f"-I{INCLUDE}",
 ]
 

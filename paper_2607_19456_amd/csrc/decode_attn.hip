@@ -32,6 +32,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <algorithm>
 #include <cstdint>
 
 #include "decode_attn.h"
@@ -46,11 +47,27 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
 constexpr int kTileRows = 16;                        // rows per MFMA tile
 constexpr int kHeadsPerBlock = 16;                   // heads per MFMA column block
-constexpr int kSplitQuantum = kTileRows * kWaves;    // split sizes are multiples
 constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgroup
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
-constexpr int kTargetWorkgroups = kComputeUnits * 8;
+constexpr int kResidentWorkgroups = kComputeUnits * 2;  // upper bound of the resident set
+// Waves per SIMD the partial kernel is compiled for: two when one MFMA column
+// block holds the group (<= 16 heads), one when two blocks share a workgroup
+// (their accumulators would not fit twice).
+template <int NB>
+constexpr int kWavesPerSimd = 1;
+// A chunk is the rows a workgroup takes at a time: a multiple of three 16-row
+// tiles per wave (the three-tile register ring).
+constexpr int kChunkQuantum = 3 * kTileRows * kWaves;
+constexpr int kDefaultChunkRows = 768;
+// Visit slots per slab, in units of the even share of waves per slab.
+constexpr int kVisitSlack = 4;
+constexpr int64_t kMaxSlabs = 1 << 20;
+// Each slab's three scheduling counters (chunks taken, visits opened, merge
+// workgroups done) share one 128-byte line of their own: atomics on counters
+// of different slabs then never serialize on the same line.
+constexpr int kCounterStride = 32;
+constexpr int kCtr = 0, kVis = 1, kDone = 2;
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ f4 mfma_16x16x4(float a, float b, f4 c) {
@@ -201,202 +218,375 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
   }
 }
 
+// Number of cache rows of slab s = (b, KV head, head group).
+__device__ __forceinline__ int slab_rows(const int32_t* __restrict__ len, int s, int per_b,
+                                         int n_max) {
+  return rows_used(len[s / per_b], n_max);
+}
+
+__device__ __forceinline__ unsigned load_counter(const unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wave-wide search (all 64 lanes call it): the first slab at or after
+// `start` (cyclically) that still has chunks and visit slots left, looking
+// at no more than `budget` slabs.  Returns -1 if none; *seen is the number of
+// slabs examined up to and including the one returned.
+__device__ int find_open_slab(const unsigned* __restrict__ cnt,
+                              const int32_t* __restrict__ len, int start, int budget, int S,
+                              int per_b, int n_max, int C, int J, int lane, int* seen) {
+  for (int base = 0; base < budget; base += kWave) {
+    const int o = base + lane;
+    int sl = start + o;
+    if (sl >= S) sl -= S;
+    bool open = false;
+    if (o < budget) {
+      const int nch = (slab_rows(len, sl, per_b, n_max) + C - 1) / C;
+      const unsigned* c = cnt + (size_t)sl * kCounterStride;
+      open = (int)load_counter(c + kCtr) < nch && (int)load_counter(c + kVis) < J;
+    }
+    const unsigned long long m = __ballot(open);
+    if (m) {
+      const int first = __ffsll((long long)m) - 1;
+      *seen = base + first + 1;
+      const int r = start + base + first;
+      return r >= S ? r - S : r;
+    }
+  }
+  *seen = budget;
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// Partials, persistent form.
+//
+// A slab is the cache rows of one (b, KV head, head group); it is cut into
+// chunks of C rows handed out by a per-slab counter.  A fixed set of
+// workgroups (two per CU for groups of <= 16 heads) stays resident; each one
+// opens a "visit" on a slab with chunks left (slot j = vis++, at most J per
+// slab), takes chunks from that slab's counter until none are left -- its four
+// waves interleave the chunk's 16-row tiles, so the workgroup streams one
+// contiguous run of K and of V -- and folds all of them into one running
+// (max, sum, weighted sum) state, since the online softmax does not care which
+// rows it has seen.  It then writes one partial for the visit to slot j and
+// looks for the next slab.  No CU idles while rows remain and faster CUs
+// simply take more chunks.
+//
+//   counters   per slab {ctr, vis, done}, one 128-byte line each; zero on
+//              entry, reset by the merge
+//   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum);
+//                                        max = -inf marks a visit that got no rows
+//   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
+// ---------------------------------------------------------------------------
 template <int DK, int DV, int NB>
-__global__ __launch_bounds__(kThreads) void decode_partial_kernel(
+__global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_kernel(
     const float* __restrict__ q, const float* __restrict__ K,
     const float* __restrict__ V, const int32_t* __restrict__ len,
-    float qscale, int h_q, int h_kv, int n_max, int split_rows, int P,
-    int head_groups, float2* __restrict__ ws_ml, float* __restrict__ ws_acc) {
-  const int p = blockIdx.x;
-  const int g = blockIdx.y / head_groups;
-  const int hgrp = blockIdx.y - g * head_groups;
-  const int b = blockIdx.z;
-
-  const int n_b = rows_used(len[b], n_max);
-  const int row_begin = p * split_rows;
-  if (row_begin >= n_b) return;                       // whole workgroup exits
-  const int row_end = min(row_begin + split_rows, n_b);
-  const int last_row = row_end - 1;
-
+    float qscale, int B, int h_q, int h_kv, int n_max, int C, int head_groups, int J,
+    unsigned* __restrict__ cnt, float2* __restrict__ ws_ml, float* __restrict__ ws_acc) {
+  const int per_b = h_kv * head_groups;
+  const int S = B * per_b;
   const int G = h_q / h_kv;
-  const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
-  const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
+  const int tpw = C / (kTileRows * kWaves);             // tiles per wave per chunk (even)
 
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
   const int i = lane & 15;
   const int k = lane >> 4;
 
-  const int64_t slab = (int64_t)b * h_kv + g;
-  const float* __restrict__ Ks = K + slab * n_max * DK;
-  const float* __restrict__ Vs = V + slab * n_max * DV;
-
-  // B operand of the score product, staged in LDS in register order: entry
-  // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
-  // base-2 units (zero for the padding heads of a partial column block).
+  __shared__ int sh_ctl[4];                             // slab, visit slot, chunk, next chunk
+  __shared__ int sh_next[2];                            // chunk after next, by parity
   __shared__ f4 sh_q[NB][DK / 16][kWave];
-  for (int e = threadIdx.x; e < NB * (DK / 16) * kWave; e += kThreads) {
-    const int ln = e % kWave;
-    const int t = (e / kWave) % (DK / 16);
-    const int nb = e / (kWave * (DK / 16));
-    const int hl = nb * kHeadsPerBlock + (ln & 15);
-    f4 v = f4{0.f, 0.f, 0.f, 0.f};
-    if (hl < h_count)
-      v = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4)) * qscale;
-    sh_q[nb][t][ln] = v;
-  }
-  __syncthreads();
-
-  // Running state per column block; lane (k, i) belongs to head i.
-  float m_run[NB], l_run[NB];
-  f4 acc[NB][DV / 64][4];   // acc[nb][c][e][r] = O[dim 64c+16k+4r+e][head i]
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    m_run[nb] = -INFINITY;
-    l_run[nb] = 0.f;
-#pragma unroll
-    for (int c = 0; c < DV / 64; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[nb][c][e] = f4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  const int n_tiles = (row_end - row_begin + kTileRows - 1) / kTileRows;
-  // Two register tiles in ping-pong: the next tile's loads are in flight
-  // while the current one is on the matrix cores.
-  Tile<DK, DV, NB> ta, tb;
-  int tile = wave;
-  if (tile < n_tiles) load_tile(ta, Ks, Vs, row_begin + tile * kTileRows, last_row, i, k);
-  while (tile < n_tiles) {
-    if (tile + kWaves < n_tiles)
-      load_tile(tb, Ks, Vs, row_begin + (tile + kWaves) * kTileRows, last_row, i, k);
-    process_tile<DK, DV, NB>(ta, row_begin + tile * kTileRows, last_row, k, lane, sh_q, m_run, l_run, acc);
-    tile += kWaves;
-    if (tile >= n_tiles) break;
-    if (tile + kWaves < n_tiles)
-      load_tile(ta, Ks, Vs, row_begin + (tile + kWaves) * kTileRows, last_row, i, k);
-    process_tile<DK, DV, NB>(tb, row_begin + tile * kTileRows, last_row, k, lane, sh_q, m_run, l_run, acc);
-    tile += kWaves;
-  }
-
-  // Row sums of head i are spread over the 4 row groups k.
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    l_run[nb] += __shfl_xor(l_run[nb], 16);
-    l_run[nb] += __shfl_xor(l_run[nb], 32);
-  }
-
-  // Combine the 4 waves: waves 1..3 park their state in LDS in their own
-  // register layout; wave 0 rescales and adds it lane by lane.
   __shared__ f4 sh_acc[kWaves - 1][NB][DV / 64][4][kWave];
   __shared__ float sh_m[kWaves - 1][NB][kWave];
   __shared__ float sh_l[kWaves - 1][NB][kWave];
-  if (wave > 0) {
+
+  int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
+
+  while (true) {
+    // ---- wave 0 opens a visit: a slab with chunks and slots left, its visit
+    // slot and its first two chunks (lane 0 does the atomics).
+    if (wave == 0) {
+      int s = -1, j = -1, c = -1, cn = -1;
+      int budget = S;
+      while (budget > 0) {
+        int seen;
+        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, C, J, lane,
+                                        &seen);
+        if (cand < 0) break;
+        budget -= seen;
+        start = cand + 1 == S ? 0 : cand + 1;
+        const int nch = (slab_rows(len, cand, per_b, n_max) + C - 1) / C;
+        int slot = -1, got = -1, nxt = -1;
+        if (lane == 0) {
+          unsigned* cc = cnt + (size_t)cand * kCounterStride;
+          slot = (int)atomicAdd(cc + kVis, 1u);
+          if (slot < J) {
+            got = (int)atomicAdd(cc + kCtr, 1u);
+            nxt = got < nch ? (int)atomicAdd(cc + kCtr, 1u) : nch;
+          }
+        }
+        slot = __shfl(slot, 0);
+        if (slot >= J) continue;                        // slab full of visitors
+        got = __shfl(got, 0);
+        if (got >= nch) {
+          // The slot is ours but the chunks ran out meanwhile: mark it empty.
+          const int b = cand / per_b;
+          const int rem = cand - b * per_b;
+          const int g = rem / head_groups;
+          const int hgrp = rem - g * head_groups;
+          const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
+          if (lane < h_count) {
+            const int h = g * G + hgrp * (NB * kHeadsPerBlock) + lane;
+            ws_ml[((int64_t)b * h_q + h) * J + slot] = make_float2(-INFINITY, 0.f);
+          }
+          continue;
+        }
+        s = cand; j = slot; c = got; cn = __shfl(nxt, 0);
+        break;
+      }
+      if (lane == 0) { sh_ctl[0] = s; sh_ctl[1] = j; sh_ctl[2] = c; sh_ctl[3] = cn; }
+    }
+    __syncthreads();
+    const int s = sh_ctl[0];
+    const int j = sh_ctl[1];
+    int c = sh_ctl[2];
+    int cn = sh_ctl[3];
+    if (s < 0) break;                                   // every slab is exhausted
+
+    const int b = s / per_b;
+    const int rem = s - b * per_b;
+    const int g = rem / head_groups;
+    const int hgrp = rem - g * head_groups;
+    const int n = slab_rows(len, s, per_b, n_max);
+    const int nch = (n + C - 1) / C;
+    const int last_row = n - 1;
+    const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
+    const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
+    const int64_t slab = (int64_t)b * h_kv + g;
+    const float* __restrict__ Ks = K + slab * n_max * DK;
+    const float* __restrict__ Vs = V + slab * n_max * DV;
+
+    // B operand of the score product, staged in LDS in register order: entry
+    // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
+    // base-2 units (zero for the padding heads of a partial column block).
+    for (int e = tid; e < NB * (DK / 16) * kWave; e += kThreads) {
+      const int ln = e % kWave;
+      const int t = (e / kWave) % (DK / 16);
+      const int nb = e / (kWave * (DK / 16));
+      const int hl = nb * kHeadsPerBlock + (ln & 15);
+      f4 v = f4{0.f, 0.f, 0.f, 0.f};
+      if (hl < h_count)
+        v = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4)) * qscale;
+      sh_q[nb][t][ln] = v;
+    }
+    __syncthreads();
+
+    // Running state per column block; lane (k, i) belongs to head i.
+    float m_run[NB], l_run[NB];
+    f4 acc[NB][DV / 64][4];   // acc[nb][c][e][r] = O[dim 64c+16k+4r+e][head i]
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      sh_m[wave - 1][nb][lane] = m_run[nb];
-      sh_l[wave - 1][nb][lane] = l_run[nb];
+      m_run[nb] = -INFINITY;
+      l_run[nb] = 0.f;
 #pragma unroll
-      for (int c = 0; c < DV / 64; ++c)
+      for (int cc = 0; cc < DV / 64; ++cc)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sh_acc[wave - 1][nb][c][e][lane] = acc[nb][c][e];
-    }
-  }
-  __syncthreads();
-  if (wave != 0) return;
-
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    float M = m_run[nb];
-#pragma unroll
-    for (int w = 0; w < kWaves - 1; ++w) M = fmaxf(M, sh_m[w][nb][lane]);
-    const float w0 = fast_exp2(m_run[nb] - M);
-    float L = l_run[nb] * w0;
-#pragma unroll
-    for (int c = 0; c < DV / 64; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[nb][c][e] *= w0;
-#pragma unroll
-    for (int w = 0; w < kWaves - 1; ++w) {
-      const float ww = fast_exp2(sh_m[w][nb][lane] - M);   // empty wave: exp2(-inf) = 0
-      L += sh_l[w][nb][lane] * ww;
-#pragma unroll
-      for (int c = 0; c < DV / 64; ++c)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[nb][c][e] += sh_acc[w][nb][c][e][lane] * ww;
+        for (int e = 0; e < 4; ++e) acc[nb][cc][e] = f4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int hl = nb * kHeadsPerBlock + i;
-    if (hl < h_count) {
-      const int64_t slot = ((int64_t)b * h_q + h_first + hl) * P + p;
-      if (k == 0) ws_ml[slot] = make_float2(M, L);
-      float* dst = ws_acc + slot * DV;
+    // The wave's tiles of chunk x: rows x*C + (4t + wave)*16, t < tpw.  Two
+    // register tiles in ping-pong keep the next tile's loads in flight while
+    // the current one is on the matrix cores, across chunk boundaries too;
+    // the chunk after next is requested at the start of each chunk.
+    // Three register tiles in a ring: while one tile is on the matrix cores
+    // the loads of the next two are in flight, across chunk boundaries too
+    // (tile x of the wave's sequence: x < tpw in this chunk, then the next
+    // chunk's; past the visit's end the clamped last row, already cached, is
+    // loaded so every path keeps the same loads in flight).  The chunk after
+    // next is requested at the start of each chunk.
+    auto row_of = [&](int x, int cc, int cnn) {
+      return x < tpw ? cc * C + x * (kWaves * kTileRows) + wave * kTileRows
+                     : (cnn < nch ? cnn * C + (x - tpw) * (kWaves * kTileRows) + wave * kTileRows
+                                  : last_row);
+    };
+    Tile<DK, DV, NB> t0, t1, t2;
+    load_tile(t0, Ks, Vs, row_of(0, c, cn), last_row, i, k);
+    load_tile(t1, Ks, Vs, row_of(1, c, cn), last_row, i, k);
+    for (int it = 0;; ++it) {
+      // Thread 0 asks for the chunk after next even on the last chunk (the
+      // counter simply runs past the end): a conditional request would merge
+      // its result with another value right here and force a wait for it.
+      int after;
+      if (tid == 0) after = (int)atomicAdd(cnt + (size_t)s * kCounterStride + kCtr, 1u);
+      // A loop that always runs at least once and exits at its bottom: after
+      // its first wait on a tile load the compiler knows the atomic issued
+      // above (an older memory operation) has returned, so publishing its
+      // value below costs no wait that would drain the prefetched tiles.
+      int t = 0;
+      do {
+        const int r0 = row_of(t, c, cn);
+        const int r1 = row_of(t + 1, c, cn);
+        const int r2 = row_of(t + 2, c, cn);
+        load_tile(t2, Ks, Vs, r2, last_row, i, k);
+        if (r0 <= last_row && t < tpw)
+          process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
+        load_tile(t0, Ks, Vs, row_of(t + 3, c, cn), last_row, i, k);
+        if (r1 <= last_row && t + 1 < tpw)
+          process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
+        load_tile(t1, Ks, Vs, row_of(t + 4, c, cn), last_row, i, k);
+        if (r2 <= last_row && t + 2 < tpw)
+          process_tile<DK, DV, NB>(t2, r2, last_row, k, lane, sh_q, m_run, l_run, acc);
+        t += 3;
+      } while (t < tpw);
+      if (tid == 0) sh_next[it & 1] = after;
+      __syncthreads();
+      if (cn >= nch) break;
+      c = cn;
+      cn = sh_next[it & 1];
+    }
+
+    // Row sums of head i are spread over the 4 row groups k.
 #pragma unroll
-      for (int c = 0; c < DV / 64; ++c)
+    for (int nb = 0; nb < NB; ++nb) {
+      l_run[nb] += __shfl_xor(l_run[nb], 16);
+      l_run[nb] += __shfl_xor(l_run[nb], 32);
+    }
+
+    // Combine the 4 waves: waves 1..3 park their state in LDS in their own
+    // register layout; wave 0 rescales and adds it lane by lane.
+    if (wave > 0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const f4 o = f4{acc[nb][c][0][r], acc[nb][c][1][r], acc[nb][c][2][r], acc[nb][c][3][r]};
-          *reinterpret_cast<f4*>(dst + 64 * c + 16 * k + 4 * r) = o;
+      for (int nb = 0; nb < NB; ++nb) {
+        sh_m[wave - 1][nb][lane] = m_run[nb];
+        sh_l[wave - 1][nb][lane] = l_run[nb];
+#pragma unroll
+        for (int cc = 0; cc < DV / 64; ++cc)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sh_acc[wave - 1][nb][cc][e][lane] = acc[nb][cc][e];
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        // Wave 0 always holds the visit's first row, so M is finite; a wave
+        // that saw no row has m = -inf and weight exp2(-inf) = 0.
+        float M = m_run[nb];
+#pragma unroll
+        for (int w = 0; w < kWaves - 1; ++w) M = fmaxf(M, sh_m[w][nb][lane]);
+        const float w0 = fast_exp2(m_run[nb] - M);
+        float L = l_run[nb] * w0;
+#pragma unroll
+        for (int cc = 0; cc < DV / 64; ++cc)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[nb][cc][e] *= w0;
+#pragma unroll
+        for (int w = 0; w < kWaves - 1; ++w) {
+          const float ww = fast_exp2(sh_m[w][nb][lane] - M);
+          L += sh_l[w][nb][lane] * ww;
+#pragma unroll
+          for (int cc = 0; cc < DV / 64; ++cc)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[nb][cc][e] += sh_acc[w][nb][cc][e][lane] * ww;
         }
+        const int hl = nb * kHeadsPerBlock + i;
+        if (hl < h_count) {
+          const int64_t slot = ((int64_t)b * h_q + h_first + hl) * J + j;
+          if (k == 0) ws_ml[slot] = make_float2(M, L);
+          float* dst = ws_acc + slot * DV;
+#pragma unroll
+          for (int cc = 0; cc < DV / 64; ++cc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const f4 o = f4{acc[nb][cc][0][r], acc[nb][cc][1][r], acc[nb][cc][2][r],
+                              acc[nb][cc][3][r]};
+              *reinterpret_cast<f4*>(dst + 64 * cc + 16 * k + 4 * r) = o;
+            }
+        }
+      }
     }
+    // Wave 0 runs the next search; the barrier at its end keeps the other
+    // waves from touching sh_q / sh_ctl before wave 0 is done here.
   }
 }
 
 // ---------------------------------------------------------------------------
-// Merge: out[b,h,:] = sum_p 2^(m_p - M) acc_p / sum_p 2^(m_p - M) l_p.
-// One workgroup per (b, h); thread = (16-byte column chunk, split subset).
+// Merge, one workgroup per (slab, query head of its group):
+//   out[b,h,:] = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j
+// over the slab's min(vis[s], J) visit partials (empty visits, m = -inf, are
+// skipped).  Threads split the visits 8 ways and the 16-byte columns 32 ways
+// (d_v = 128), then combine through LDS.  The last workgroup of a slab to
+// finish resets the slab's three counters to zero for the next call.
 // ---------------------------------------------------------------------------
 template <int DV>
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
-    const int32_t* __restrict__ len, float* __restrict__ out,
-    const float2* __restrict__ ws_ml, const float* __restrict__ ws_acc,
-    int h_q, int n_max, int split_rows, int P) {
-  constexpr int kChunks = DV / 4;
-  constexpr int kLanesP = kThreads / kChunks;       // splits visited in parallel
-  const int bh = blockIdx.x;
-  const int b = bh / h_q;
-  const int n_b = rows_used(len[b], n_max);
-  const int Pb = (n_b + split_rows - 1) / split_rows;
+    float* __restrict__ out, const float2* __restrict__ ws_ml,
+    const float* __restrict__ ws_acc, int h_q, int h_kv, int head_groups, int heads_per_group,
+    int merge_heads, int J, unsigned* __restrict__ cnt) {
+  constexpr int kChunks = DV / 4;                       // 16-byte columns per row
+  constexpr int kLanesV = kThreads / kChunks;           // visits merged in parallel
+  const int s = blockIdx.x / merge_heads;
+  const int hl = blockIdx.x - s * merge_heads;
+  const int per_b = h_kv * head_groups;
+  const int b = s / per_b;
+  const int rem = s - b * per_b;
+  const int g = rem / head_groups;
+  const int hgrp = rem - g * head_groups;
+  const int G = h_q / h_kv;
+  const int h_count = min(heads_per_group, G - hgrp * heads_per_group);
+  if (hl >= h_count) return;                            // padding workgroup
+  unsigned* slab_cnt = cnt + (size_t)s * kCounterStride;
+  const int nv = min((int)slab_cnt[kVis], J);
   const int ch = threadIdx.x % kChunks;
-  const int ps = threadIdx.x / kChunks;
-  float* orow = out + (int64_t)bh * DV;
-  if (Pb == 0) {                                      // empty cache: zeros
-    if (ps == 0) *reinterpret_cast<f4*>(orow + 4 * ch) = f4{0.f, 0.f, 0.f, 0.f};
-    return;
-  }
-  const float2* ml = ws_ml + (int64_t)bh * P;
-  const float* acc = ws_acc + (int64_t)bh * P * DV;
+  const int pv = threadIdx.x / kChunks;
+  const int64_t row = (int64_t)b * h_q + g * G + hgrp * heads_per_group + hl;
+  const float2* ml = ws_ml + row * J;
+  const float* acc = ws_acc + row * J * DV;
 
-  __shared__ float sh_red[kThreads];
-  float m = -INFINITY;
-  for (int pp = threadIdx.x; pp < Pb; pp += kThreads) m = fmaxf(m, ml[pp].x);
-  sh_red[threadIdx.x] = m;
-  __syncthreads();
-  for (int s = kThreads / 2; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) sh_red[threadIdx.x] = fmaxf(sh_red[threadIdx.x], sh_red[threadIdx.x + s]);
-    __syncthreads();
-  }
-  const float M = sh_red[0];
-  __syncthreads();
-
+  float m = -INFINITY, l = 0.f;
   f4 o = f4{0.f, 0.f, 0.f, 0.f};
-  float L = 0.f;
-  for (int pp = ps; pp < Pb; pp += kLanesP) {
-    const float2 st = ml[pp];
-    const float w = fast_exp2(st.x - M);
-    L += st.y * w;
-    o += load4(acc + (int64_t)pp * DV + 4 * ch) * w;
+  for (int jj = pv; jj < nv; jj += kLanesV) {
+    const float2 st = ml[jj];
+    if (st.x == -INFINITY) continue;                    // an empty visit
+    const float mn = fmaxf(m, st.x);
+    const float a = fast_exp2(m - mn);                  // m = -inf: 0
+    const float w = fast_exp2(st.x - mn);
+    l = l * a + st.y * w;
+    o = o * a + load4(acc + (int64_t)jj * DV + 4 * ch) * w;
+    m = mn;
   }
+  __shared__ float sh_m[kThreads], sh_l[kThreads];
   __shared__ f4 sh_o[kThreads];
-  __shared__ float sh_l[kThreads];
+  sh_m[threadIdx.x] = m;
+  sh_l[threadIdx.x] = l;
   sh_o[threadIdx.x] = o;
-  sh_l[threadIdx.x] = L;
   __syncthreads();
-  if (ps == 0) {
-    for (int j = 1; j < kLanesP; ++j) {
-      o += sh_o[j * kChunks + ch];
-      L += sh_l[j * kChunks + ch];
+  if (pv == 0) {
+    float M = m;
+    for (int p = 1; p < kLanesV; ++p) M = fmaxf(M, sh_m[p * kChunks + ch]);
+    float L = 0.f;
+    f4 O = f4{0.f, 0.f, 0.f, 0.f};
+    if (M != -INFINITY) {
+      for (int p = 0; p < kLanesV; ++p) {
+        const float w = fast_exp2(sh_m[p * kChunks + ch] - M);
+        L += sh_l[p * kChunks + ch] * w;
+        O += sh_o[p * kChunks + ch] * w;
+      }
     }
-    *reinterpret_cast<f4*>(orow + 4 * ch) = o / L;
+    // No visit (empty cache): the output row is zero.
+    *reinterpret_cast<f4*>(out + row * DV + 4 * ch) = M != -INFINITY ? O / L : f4{0.f, 0.f, 0.f, 0.f};
+  }
+  if (threadIdx.x == 0) {
+    // Every workgroup of the slab read vis[s] above (nv is already in use);
+    // the last one to get here clears the slab's counters.
+    __threadfence();
+    if (atomicAdd(slab_cnt + kDone, 1u) == (unsigned)h_count - 1u) {
+      slab_cnt[kVis] = 0u;
+      slab_cnt[kCtr] = 0u;
+      slab_cnt[kDone] = 0u;
+    }
   }
 }
 
@@ -404,56 +594,72 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
 // Host side: validation, sizing, launches.
 // ---------------------------------------------------------------------------
 struct Plan {
-  int split_rows;
-  int P;             // splits per slab
-  int head_groups;   // workgroups per KV head along the head axis
-  int blocks;        // MFMA column blocks per workgroup (1 or 2)
-  size_t ml_bytes;   // bytes of the (max, sum) section, padded to 256
-  size_t bytes;      // total workspace bytes
+  int chunk_rows;     // rows per dynamically scheduled chunk (one wave's unit)
+  int head_groups;    // groups of up to 32 query heads per KV head
+  int blocks;         // MFMA column blocks per wave (1 or 2)
+  int slabs;          // B * h_kv * head_groups
+  int grid;           // resident workgroups of the partial kernel
+  int J;              // visit slots per (b, query head)
+  int merge_heads;    // query heads per slab the merge covers
+  size_t counter_bytes, ml_bytes, bytes;
 };
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 bool dim_ok(int d) { return d == 64 || d == 128; }
-
-int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t pad256(size_t x) { return (x + 255) / 256 * 256; }
 
 da_status check_shapes(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
   if (B < 1 || h_q < 1 || h_kv < 1 || n_max < 1 || d_k < 1 || d_v < 1) return DA_ERR_SHAPE;
   if (h_q % h_kv != 0) return DA_ERR_SHAPE;
-  if (B > 65535) return DA_ERR_SHAPE;
-  const int G = h_q / h_kv;
-  const int64_t groups = (int64_t)h_kv * ceil_div(G, kHeadsPerGroup);
-  if (groups > 65535) return DA_ERR_SHAPE;
+  const int64_t slabs = (int64_t)B * h_kv * ceil_div(h_q / h_kv, kHeadsPerGroup);
+  if (slabs > kMaxSlabs || (int64_t)B * h_q > kMaxSlabs * kHeadsPerGroup) return DA_ERR_SHAPE;
   if (!dim_ok(d_k) || !dim_ok(d_v)) return DA_ERR_UNSUPPORTED;
   return DA_OK;
 }
 
-int auto_split_rows(int B, int h_q, int h_kv, int n_max) {
-  const int G = h_q / h_kv;
-  const int64_t units = (int64_t)B * h_kv * ceil_div(G, kHeadsPerGroup);
-  const int64_t rows = (units * n_max + kTargetWorkgroups - 1) / kTargetWorkgroups;
-  int64_t s = ((rows + kSplitQuantum - 1) / kSplitQuantum) * kSplitQuantum;
-  if (s < kSplitQuantum) s = kSplitQuantum;
-  const int64_t cap = ((int64_t)n_max + kSplitQuantum - 1) / kSplitQuantum * kSplitQuantum;
-  if (s > cap) s = cap;
-  return (int)s;
-}
-
-da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int split_rows,
+da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
                     Plan* plan) {
   da_status st = check_shapes(B, h_q, h_kv, n_max, d_k, d_v);
   if (st != DA_OK) return st;
-  if (split_rows == 0) split_rows = auto_split_rows(B, h_q, h_kv, n_max);
-  if (split_rows < kSplitQuantum || split_rows % kSplitQuantum != 0) return DA_ERR_SHAPE;
+  if (chunk_rows == 0) chunk_rows = kDefaultChunkRows;
+  if (chunk_rows < kChunkQuantum || chunk_rows % kChunkQuantum != 0) return DA_ERR_SHAPE;
   const int G = h_q / h_kv;
-  plan->split_rows = split_rows;
-  plan->P = ceil_div(n_max, split_rows);
-  plan->head_groups = ceil_div(G, kHeadsPerGroup);
+  plan->chunk_rows = chunk_rows;
+  plan->head_groups = (int)ceil_div(G, kHeadsPerGroup);
   plan->blocks = G > kHeadsPerBlock ? 2 : 1;
-  const size_t slots = (size_t)B * h_q * plan->P;
-  plan->ml_bytes = (slots * sizeof(float2) + 255) / 256 * 256;
-  plan->bytes = plan->ml_bytes + slots * (size_t)d_v * sizeof(float);
+  plan->slabs = B * h_kv * plan->head_groups;
+  plan->merge_heads = std::min(G, plan->blocks * kHeadsPerBlock);
+  const int64_t chunks_per_slab = ceil_div(n_max, chunk_rows);
+  // One resident workgroup per CU and wave slot, fewer if there are fewer
+  // chunks than that.
+  const int64_t resident = (int64_t)kComputeUnits;
+  plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
+  // A slab is visited at most once per workgroup and per chunk; kVisitSlack
+  // times the even share of workgroups per slab leaves room for workgroups
+  // that move on from finished slabs.
+  const int64_t share = ceil_div((int64_t)plan->grid, plan->slabs);
+  plan->J = (int)std::max<int64_t>(1, std::min(chunks_per_slab, kVisitSlack * share));
+  const size_t slots = (size_t)B * h_q * plan->J;
+  plan->counter_bytes = pad256((size_t)plan->slabs * kCounterStride * sizeof(unsigned));
+  plan->ml_bytes = pad256(slots * sizeof(float2));
+  plan->bytes = plan->counter_bytes + plan->ml_bytes + slots * (size_t)d_v * sizeof(float);
   return DA_OK;
+}
+
+struct WsView {
+  unsigned* cnt;
+  float2* ml;
+  float* acc;
+};
+
+WsView view(const Plan& pl, void* workspace) {
+  char* base = static_cast<char*>(workspace);
+  WsView w;
+  w.cnt = reinterpret_cast<unsigned*>(base);
+  w.ml = reinterpret_cast<float2*>(base + pl.counter_bytes);
+  w.acc = reinterpret_cast<float*>(base + pl.counter_bytes + pl.ml_bytes);
+  return w;
 }
 
 da_status launch_status() {
@@ -463,30 +669,29 @@ da_status launch_status() {
 template <int DK, int DV, int NB>
 void launch_partial(const Plan& pl, const float* q, const float* K, const float* V,
                     const int32_t* len, float qscale, int B, int h_q, int h_kv, int n_max,
-                    float2* ml, float* acc, hipStream_t stream) {
-  dim3 grid(pl.P, h_kv * pl.head_groups, B);
-  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB>), grid, dim3(kThreads), 0, stream,
-                     q, K, V, len, qscale, h_q, h_kv, n_max, pl.split_rows, pl.P,
-                     pl.head_groups, ml, acc);
+                    const WsView& w, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB>), dim3(pl.grid), dim3(kThreads), 0,
+                     stream, q, K, V, len, qscale, B, h_q, h_kv, n_max, pl.chunk_rows,
+                     pl.head_groups, pl.J, w.cnt, w.ml, w.acc);
 }
 
 template <int DK, int DV>
 void launch_partial_nb(const Plan& pl, const float* q, const float* K, const float* V,
                        const int32_t* len, float qscale, int B, int h_q, int h_kv,
-                       int n_max, float2* ml, float* acc, hipStream_t s) {
+                       int n_max, const WsView& w, hipStream_t s) {
   if (pl.blocks == 1)
-    launch_partial<DK, DV, 1>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
+    launch_partial<DK, DV, 1>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
   else
-    launch_partial<DK, DV, 2>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
+    launch_partial<DK, DV, 2>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
 }
 
 da_status partial_impl(const float* q, const float* K, const float* V, const int32_t* len,
                        float scale, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                       int split_rows, void* workspace, size_t workspace_bytes,
+                       int chunk_rows, void* workspace, size_t workspace_bytes,
                        void* stream, Plan* out_plan) {
   if (!q || !K || !V || !len) return DA_ERR_NULL;
   Plan pl;
-  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, split_rows, &pl);
+  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4))
     return DA_ERR_ALIGN;
@@ -495,41 +700,38 @@ da_status partial_impl(const float* q, const float* K, const float* V, const int
   if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
   if (out_plan) *out_plan = pl;
 
-  float2* ml = static_cast<float2*>(workspace);
-  float* acc = reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.ml_bytes);
+  const WsView w = view(pl, workspace);
   const float qscale = scale * kLog2e;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
-  else if (d_k == 64 && d_v == 128) launch_partial_nb<64, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
-  else if (d_k == 128 && d_v == 64) launch_partial_nb<128, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
-  else launch_partial_nb<128, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, ml, acc, s);
+  if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+  else if (d_k == 64 && d_v == 128) launch_partial_nb<64, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+  else if (d_k == 128 && d_v == 64) launch_partial_nb<128, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+  else launch_partial_nb<128, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
   return launch_status();
 }
 
-da_status merge_impl(const int32_t* len, float* out, int B, int h_q, int h_kv, int n_max,
-                     int d_k, int d_v, int split_rows, const void* workspace,
-                     size_t workspace_bytes, void* stream) {
-  if (!len || !out) return DA_ERR_NULL;
+da_status merge_impl(float* out, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
+                     int chunk_rows, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!out) return DA_ERR_NULL;
   Plan pl;
-  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, split_rows, &pl);
+  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
-  if (!aligned(out, 16) || !aligned(len, 4)) return DA_ERR_ALIGN;
+  if (!aligned(out, 16)) return DA_ERR_ALIGN;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
 
-  const float2* ml = static_cast<const float2*>(workspace);
-  const float* acc =
-      reinterpret_cast<const float*>(static_cast<const char*>(workspace) + pl.ml_bytes);
+  const WsView w = view(pl, workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  const dim3 grid((unsigned)B * (unsigned)h_q);
+  const int heads_per_group = pl.blocks * kHeadsPerBlock;
+  const dim3 grid((unsigned)pl.slabs * (unsigned)pl.merge_heads);
   if (d_v == 64)
-    hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, len, out, ml, acc,
-                       h_q, n_max, pl.split_rows, pl.P);
+    hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
+                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(kThreads), 0, s, len, out, ml,
-                       acc, h_q, n_max, pl.split_rows, pl.P);
+    hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
+                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt);
   return launch_status();
 }
 
@@ -541,7 +743,7 @@ const char* da_status_string(int status) {
   switch (status) {
     case DA_OK: return "DA_OK";
     case DA_ERR_NULL: return "DA_ERR_NULL: a required pointer is NULL";
-    case DA_ERR_SHAPE: return "DA_ERR_SHAPE: invalid sizes or split_rows";
+    case DA_ERR_SHAPE: return "DA_ERR_SHAPE: invalid sizes or chunk_rows";
     case DA_ERR_UNSUPPORTED: return "DA_ERR_UNSUPPORTED: head dimension not supported";
     case DA_ERR_ALIGN: return "DA_ERR_ALIGN: pointer not aligned";
     case DA_ERR_SCALE: return "DA_ERR_SCALE: scale is not finite";
@@ -551,51 +753,58 @@ const char* da_status_string(int status) {
   }
 }
 
-int da_decode_split_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
+int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
   Plan pl;
   if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, &pl) != DA_OK) return 0;
-  return pl.split_rows;
+  return pl.chunk_rows;
 }
 
 size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                                 int split_rows) {
+                                 int chunk_rows) {
   Plan pl;
-  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, split_rows, &pl) != DA_OK) return 0;
+  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl) != DA_OK) return 0;
   return pl.bytes;
+}
+
+size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
+                                         int d_v) {
+  Plan pl;
+  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, &pl) != DA_OK) return 0;
+  return pl.counter_bytes;
 }
 
 da_status da_decode_partial(const float* q, const float* K, const float* V,
                             const int32_t* len, float scale, int B, int h_q, int h_kv,
-                            int n_max, int d_k, int d_v, int split_rows, void* workspace,
+                            int n_max, int d_k, int d_v, int chunk_rows, void* workspace,
                             size_t workspace_bytes, void* stream) {
-  return partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, split_rows,
+  return partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
                       workspace, workspace_bytes, stream, nullptr);
 }
 
-da_status da_decode_merge(const int32_t* len, float* out, int B, int h_q, int h_kv,
-                          int n_max, int d_k, int d_v, int split_rows,
-                          const void* workspace, size_t workspace_bytes, void* stream) {
-  return merge_impl(len, out, B, h_q, h_kv, n_max, d_k, d_v, split_rows, workspace,
+da_status da_decode_merge(float* out, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
+                          int chunk_rows, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return merge_impl(out, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 
 da_status da_decode_attn(const float* q, const float* K, const float* V, const int32_t* len,
                          float scale, float* out, int B, int h_q, int h_kv, int n_max,
-                         int d_k, int d_v, int split_rows, void* workspace,
+                         int d_k, int d_v, int chunk_rows, void* workspace,
                          size_t workspace_bytes, void* stream) {
   if (!out) return DA_ERR_NULL;
   if (!aligned(out, 16)) {
-    // Report the full validation order of the partial first (NULL before ALIGN).
+    // Same order as the partial's checks: NULL and shape errors before ALIGN.
     if (!q || !K || !V || !len) return DA_ERR_NULL;
     Plan pl;
-    da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, split_rows, &pl);
+    da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
     return st != DA_OK ? st : DA_ERR_ALIGN;
   }
   Plan pl;
-  da_status st = partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, split_rows,
+  da_status st = partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
                               workspace, workspace_bytes, stream, &pl);
   if (st != DA_OK) return st;
-  return merge_impl(len, out, B, h_q, h_kv, n_max, d_k, d_v, pl.split_rows, workspace,
+  return merge_impl(out, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 

@@ -42,39 +42,53 @@ def test_status_strings():
     assert b"unknown" in lib.da_status_string(99)
 
 
-def test_split_rows_and_workspace_sizes():
+def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
+    """The sizing rule the header documents, restated: one visit slot per
+    (b, query head) for up to 4x the even share of resident waves per slab."""
+    pad = lambda x: -(-x // 256) * 256
+    G = h_q // h_kv
+    groups = -(-G // 32)
+    slabs = B * h_kv * groups
+    chunks = -(-n_max // c)
+    resident = 256
+    grid = max(1, min(resident, chunks * slabs))
+    J = max(1, min(chunks, 4 * -(-grid // slabs)))
+    slots = B * h_q * J
+    counters = pad(slabs * 128)
+    return counters, counters + pad(slots * 8) + slots * d_v * 4
+
+
+def test_chunk_rows_and_workspace_sizes():
     for args in [(1, 1, 1, 128, 64, 64), (8, 32, 32, 4112, 128, 128),
                  (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
                  (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]:
-        B, h_q, h_kv, n_max, d_k, d_v = args
-        s = binding.split_rows(*args)
-        assert s >= 64 and s % 64 == 0
-        P = -(-n_max // s)
-        slots = B * h_q * P
-        ml = -(-slots * 8 // 256) * 256
-        assert binding.workspace_bytes(*args) == ml + slots * d_v * 4
-        assert binding.workspace_bytes(*args, 64) >= binding.workspace_bytes(*args)
-    assert binding.split_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
+        c = binding.chunk_rows(*args)
+        assert c >= 192 and c % 192 == 0
+        counters, total = _expected_workspace(*args, c)
+        assert binding.workspace_counter_bytes(*args) == counters
+        assert binding.workspace_bytes(*args) == total
+        assert binding.workspace_bytes(*args, 192) == _expected_workspace(*args, 192)[1]
+    assert binding.chunk_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
     assert binding.workspace_bytes(1, 1, 1, 10, 96, 64) == 0  # unsupported d_k
-    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 100) == 0  # split not a multiple of 64
+    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 128) == 0  # chunk not a multiple of 192
 
 
 def _decode(**kw):
     a = dict(q=FAKE, K=FAKE, V=FAKE, len=FAKE, scale=0.125, out=FAKE, B=1, h_q=1,
-             h_kv=1, n_max=128, d_k=64, d_v=64, split=0, ws=FAKE, wsn=1 << 30,
+             h_kv=1, n_max=128, d_k=64, d_v=64, chunk=0, ws=FAKE, wsn=1 << 30,
              stream=None)
     a.update(kw)
     return lib.da_decode_attn(a["q"], a["K"], a["V"], a["len"], a["scale"], a["out"],
                               a["B"], a["h_q"], a["h_kv"], a["n_max"], a["d_k"],
-                              a["d_v"], a["split"], a["ws"], a["wsn"], a["stream"])
+                              a["d_v"], a["chunk"], a["ws"], a["wsn"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(q=None), 1), (dict(K=None), 1), (dict(V=None), 1), (dict(len=None), 1),
     (dict(out=None), 1),
     (dict(B=0), 2), (dict(h_q=0), 2), (dict(h_kv=0), 2), (dict(n_max=0), 2),
-    (dict(h_q=3, h_kv=2), 2), (dict(B=70000), 2), (dict(split=100), 2),
-    (dict(split=32), 2),
+    (dict(h_q=3, h_kv=2), 2), (dict(B=1 << 21), 2), (dict(chunk=100), 2),
+    (dict(chunk=128), 2), (dict(chunk=-192), 2),
     (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=256), 3),
     (dict(q=FAKE + 4), 4), (dict(K=FAKE + 8), 4), (dict(out=FAKE + 4), 4),
     (dict(len=FAKE + 2), 4),
@@ -93,12 +107,14 @@ def test_partial_and_merge_validation():
     p = lib.da_decode_partial(FAKE, FAKE, FAKE, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
                               FAKE, 8, None)
     assert p == 6
-    m = lib.da_decode_merge(FAKE, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
+    m = lib.da_decode_merge(None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
     assert m == 1
-    m = lib.da_decode_merge(FAKE, FAKE, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None)
+    m = lib.da_decode_merge(FAKE, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None)
     assert m == 2
-    m = lib.da_decode_merge(FAKE, FAKE, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None)
+    m = lib.da_decode_merge(FAKE, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None)
     assert m == 6
+    m = lib.da_decode_merge(FAKE + 4, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
+    assert m == 4
 
 
 @pytest.mark.parametrize("args,status", [

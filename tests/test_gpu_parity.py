@@ -26,18 +26,32 @@ def dev(a, device):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def run_decode(inp, device, q=None, lens=None, split_rows=0, K=None, V=None):
+def poisoned_workspace(dq, dK, dV, chunk_rows=0):
+    """Workspace whose partial slots hold NaN bit patterns (a decode must
+    never read a slot it did not write) and whose counters are zero."""
+    ws = binding.alloc_workspace(dq, dK, dV, chunk_rows)
+    ws.fill_(0xFF)
+    B, h_q, d_k = dq.shape
+    _, h_kv, n_max, _ = dK.shape
+    ws[:binding.workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, dV.shape[3])].zero_()
+    return ws
+
+
+def run_decode(inp, device, q=None, lens=None, chunk_rows=0, K=None, V=None):
     s = inp.shape
     q = inp.q if q is None else q
     lens = inp.lens if lens is None else lens
     dK = dev(inp.K, device) if K is None else K
     dV = dev(inp.V, device) if V is None else V
     dq, dl = dev(q, device), dev(lens, device)
-    ws = binding.alloc_workspace(dq, dK, dV, split_rows)
-    ws.view(torch.uint8).fill_(0xFF)         # NaN-poison the partials
+    ws = poisoned_workspace(dq, dK, dV, chunk_rows)
     out = binding.decode_attn(dq, dK, dV, dl, float(s.scale32()), workspace=ws,
-                              split_rows=split_rows)
+                              chunk_rows=chunk_rows)
     torch.cuda.synchronize()
+    # a completed decode leaves the counters zero for the next call
+    nc = binding.workspace_counter_bytes(*dq.shape[:2], dK.shape[1], dK.shape[2],
+                                         dq.shape[2], dV.shape[3])
+    assert not ws[:nc].any(), "counters not reset by the merge"
     return out.cpu().numpy().astype(np.float64)
 
 
@@ -69,14 +83,14 @@ SMALL = [
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
-@pytest.mark.parametrize("split_rows", [0, 64, 192])
-def test_decode_small_shapes(cuda_device, case, split_rows):
+@pytest.mark.parametrize("chunk_rows", [0, 192, 576])
+def test_decode_small_shapes(cuda_device, case, chunk_rows):
     name, B, h_q, h_kv, d_k, d_v, n_max, lens = case
     shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v,
                              n_max=n_max)
     inp = workloads.make(shape, seed=zlib.crc32(name.encode()) % 1000, lens=np.array(lens, np.int32))
-    say(f"decode {name} split_rows={split_rows} lens={lens}")
-    got = run_decode(inp, cuda_device, split_rows=split_rows)
+    say(f"decode {name} chunk_rows={chunk_rows} lens={lens}")
+    got = run_decode(inp, cuda_device, chunk_rows=chunk_rows)
     ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
     check(got, ref, name)
     for b, n in enumerate(lens):
@@ -84,12 +98,34 @@ def test_decode_small_shapes(cuda_device, case, split_rows):
             assert np.array_equal(got[b], np.zeros_like(got[b]))
 
 
-def test_split_count_invariance(cuda_device):
-    shape = workloads.custom("split", B=2, h_q=8, h_kv=2, d_k=128, d_v=128, n_max=4096)
+def test_chunk_size_invariance(cuda_device):
+    shape = workloads.custom("chunks", B=2, h_q=8, h_kv=2, d_k=128, d_v=128, n_max=4096)
     inp = workloads.make(shape, seed=5, lens=np.array([4096, 3000], np.int32))
-    outs = [run_decode(inp, cuda_device, split_rows=s) for s in (64, 512, 4096, 0)]
+    outs = [run_decode(inp, cuda_device, chunk_rows=c) for c in (192, 576, 4032, 0)]
     for o in outs[1:]:
         assert np.max(np.abs(o - outs[0])) <= 1e-6
+
+
+def test_workspace_reuse_across_calls_and_shapes(cuda_device):
+    """One workspace, many decodes in a row (counters must come back to zero
+    after each), including a smaller problem in the same buffer."""
+    shape = workloads.custom("reuse", B=3, h_q=16, h_kv=4, d_k=128, d_v=128, n_max=3000)
+    inp = workloads.make(shape, seed=11, lens=np.array([3000, 1500, 77], np.int32))
+    dq, dK, dV, dl = (dev(a, cuda_device) for a in (inp.q, inp.K, inp.V, inp.lens))
+    ws = binding.alloc_workspace(dq, dK, dV)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    for rep in range(5):
+        out = binding.decode_attn(dq, dK, dV, dl, float(shape.scale32()), workspace=ws)
+        torch.cuda.synchronize()
+        check(out.cpu().numpy().astype(np.float64), ref, f"reuse {rep}")
+    small = np.array([500, 0, 9], np.int32)
+    out = binding.decode_attn(dq[:, :8].contiguous(), dK[:, :2].contiguous(),
+                              dV[:, :2].contiguous(), dev(small, cuda_device),
+                              float(shape.scale32()), workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.decode(np.ascontiguousarray(inp.q[:, :8]), np.ascontiguousarray(inp.K[:, :2]),
+                        np.ascontiguousarray(inp.V[:, :2]), small, shape.scale32())
+    check(out.cpu().numpy().astype(np.float64), ref, "reuse smaller")
 
 
 def test_len_beyond_capacity_is_clamped(cuda_device):
@@ -124,10 +160,10 @@ def test_decode_partial_then_merge_equals_decode(cuda_device):
     shape = workloads.custom("pm", B=2, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=900)
     inp = workloads.make(shape, seed=9, lens=np.array([900, 450], np.int32))
     dq, dK, dV, dl = (dev(a, cuda_device) for a in (inp.q, inp.K, inp.V, inp.lens))
-    ws = binding.alloc_workspace(dq, dK, dV)
+    ws = poisoned_workspace(dq, dK, dV)
     out = torch.empty((2, 16, 128), device=cuda_device)
     binding.decode_partial(dq, dK, dV, dl, float(shape.scale32()), ws)
-    binding.decode_merge(dl, out, ws, 2, 16, 2, 900, 128, 128)
+    binding.decode_merge(out, ws, 2, 16, 2, 900, 128, 128)
     torch.cuda.synchronize()
     ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
     check(out.cpu().numpy().astype(np.float64), ref, "partial+merge")
