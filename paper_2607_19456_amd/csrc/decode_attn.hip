@@ -82,6 +82,11 @@ __device__ __forceinline__ f4 load4(const float* p) {
   return *reinterpret_cast<const f4*>(p);
 }
 
+// K/V rows are read exactly once per decode: stream them past the caches.
+__device__ __forceinline__ f4 load4_stream(const float* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+}
+
 __device__ __forceinline__ int rows_used(int32_t len_b, int n_max) {
   return len_b < 0 ? 0 : (len_b > n_max ? n_max : len_b);
 }
@@ -140,13 +145,13 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T,
   const int rk = min(row0 + i, last_row);
 #pragma unroll
   for (int t = 0; t < DK / 16; ++t)
-    T.k[t] = load4(Ks + (int64_t)rk * DK + 16 * t + 4 * k);
+    T.k[t] = load4_stream(Ks + (int64_t)rk * DK + 16 * t + 4 * k);
 #pragma unroll
   for (int rho = 0; rho < 4; ++rho) {
     const int rv = min(row0 + 4 * k + rho, last_row);
 #pragma unroll
     for (int c = 0; c < DV / 64; ++c)
-      T.v[rho][c] = load4(Vs + (int64_t)rv * DV + 64 * c + 4 * i);
+      T.v[rho][c] = load4_stream(Vs + (int64_t)rv * DV + 64 * c + 4 * i);
   }
 }
 
@@ -200,10 +205,14 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
     pr[3] = fast_exp2(s[3] - m_new);
     l_run[nb] = l_run[nb] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
     m_run[nb] = m_new;
+    // Once the running maxima settle, most tiles leave them unchanged
+    // (alpha = 1 in every lane): skip the rescale of the accumulators then.
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int c = 0; c < DV / 64; ++c)
+      for (int c = 0; c < DV / 64; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha;
+        for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha;
+    }
 
     // Step III: acc += V_tile^T . P over rows {rho, 4+rho, 8+rho, 12+rho}.
 #pragma unroll
