@@ -51,14 +51,19 @@ constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgr
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
 constexpr int kResidentWorkgroups = kComputeUnits * 2;  // upper bound of the resident set
-// Waves per SIMD the partial kernel is compiled for: two when one MFMA column
-// block holds the group (<= 16 heads), one when two blocks share a workgroup
-// (their accumulators would not fit twice).
+// Register tiles per wave in the load ring, and waves per SIMD, of the
+// partial kernel.  One MFMA column block (<= 16 heads): a three-tile ring at
+// one wave per SIMD keeps two tiles' loads in flight during each tile's
+// products.  Two column blocks (17..32 heads) double the matrix work per
+// tile: a two-tile ring leaves room for two waves per SIMD, so one wave's
+// products overlap the other's loads.
+template <int NB>
+constexpr int kRing = 3;
 template <int NB>
 constexpr int kWavesPerSimd = 1;
-// A chunk is the rows a workgroup takes at a time: a multiple of three 16-row
-// tiles per wave (the three-tile register ring).
-constexpr int kChunkQuantum = 3 * kTileRows * kWaves;
+// A chunk is the rows a workgroup takes at a time: a multiple of six 16-row
+// tiles per wave (whole turns of either ring).
+constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 constexpr int kDefaultChunkRows = 768;
 // Visit slots per slab, in units of the even share of waves per slab.
 constexpr int kVisitSlack = 4;
@@ -85,6 +90,28 @@ __device__ __forceinline__ f4 load4(const float* p) {
 // K/V rows are read exactly once per decode: stream them past the caches.
 __device__ __forceinline__ f4 load4_stream(const float* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+}
+
+// Reductions over the four 16-lane row groups of a wave (lanes i, i+16,
+// i+32, i+48 hold the same head in the score layout).  permlane16_swap(x, x)
+// returns the row pairs (r0,r0,r2,r2) and (r1,r1,r3,r3), permlane32_swap the
+// halves (lo,lo) and (hi,hi): two VALU swaps instead of two LDS shuffles.
+__device__ __forceinline__ float max_over_row_groups(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const unsigned v = __float_as_uint(m);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float sum_over_row_groups(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const unsigned v = __float_as_uint(m);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 __device__ __forceinline__ int rows_used(int32_t len_b, int n_max) {
@@ -193,9 +220,7 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
       if (row0 + 4 * k + r > last_row) s[r] = -INFINITY;
 
     // Step II, online: running max over the 4 row groups of head i.
-    float tmax = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float tmax = max_over_row_groups(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
     const float m_new = fmaxf(m_run[nb], tmax);
     const float alpha = fast_exp2(m_run[nb] - m_new);
     f4 pr;
@@ -405,13 +430,10 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
         for (int e = 0; e < 4; ++e) acc[nb][cc][e] = f4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // The wave's tiles of chunk x: rows x*C + (4t + wave)*16, t < tpw.  Two
-    // register tiles in ping-pong keep the next tile's loads in flight while
-    // the current one is on the matrix cores, across chunk boundaries too;
-    // the chunk after next is requested at the start of each chunk.
-    // Three register tiles in a ring: while one tile is on the matrix cores
-    // the loads of the next two are in flight, across chunk boundaries too
-    // (tile x of the wave's sequence: x < tpw in this chunk, then the next
+    // The wave's tiles of chunk x: rows x*C + (4t + wave)*16, t < tpw.  The
+    // register tiles form a ring: while one tile is on the matrix cores the
+    // loads of the next one or two are in flight, across chunk boundaries
+    // too (tile x of the wave's sequence: x < tpw in this chunk, then the next
     // chunk's; past the visit's end the clamped last row, already cached, is
     // loaded so every path keeps the same loads in flight).  The chunk after
     // next is requested at the start of each chunk.
@@ -422,7 +444,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     };
     Tile<DK, DV, NB> t0, t1, t2;
     load_tile(t0, Ks, Vs, row_of(0, c, cn), last_row, i, k);
-    load_tile(t1, Ks, Vs, row_of(1, c, cn), last_row, i, k);
+    if constexpr (kRing<NB> == 3) load_tile(t1, Ks, Vs, row_of(1, c, cn), last_row, i, k);
     for (int it = 0;; ++it) {
       // Thread 0 asks for the chunk after next even on the last chunk (the
       // counter simply runs past the end): a conditional request would merge
@@ -435,19 +457,31 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       // value below costs no wait that would drain the prefetched tiles.
       int t = 0;
       do {
-        const int r0 = row_of(t, c, cn);
-        const int r1 = row_of(t + 1, c, cn);
-        const int r2 = row_of(t + 2, c, cn);
-        load_tile(t2, Ks, Vs, r2, last_row, i, k);
-        if (r0 <= last_row && t < tpw)
-          process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
-        load_tile(t0, Ks, Vs, row_of(t + 3, c, cn), last_row, i, k);
-        if (r1 <= last_row && t + 1 < tpw)
-          process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
-        load_tile(t1, Ks, Vs, row_of(t + 4, c, cn), last_row, i, k);
-        if (r2 <= last_row && t + 2 < tpw)
-          process_tile<DK, DV, NB>(t2, r2, last_row, k, lane, sh_q, m_run, l_run, acc);
-        t += 3;
+        if constexpr (kRing<NB> == 3) {
+          const int r0 = row_of(t, c, cn);
+          const int r1 = row_of(t + 1, c, cn);
+          const int r2 = row_of(t + 2, c, cn);
+          load_tile(t2, Ks, Vs, r2, last_row, i, k);
+          if (r0 <= last_row)
+            process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
+          load_tile(t0, Ks, Vs, row_of(t + 3, c, cn), last_row, i, k);
+          if (r1 <= last_row)
+            process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
+          load_tile(t1, Ks, Vs, row_of(t + 4, c, cn), last_row, i, k);
+          if (r2 <= last_row)
+            process_tile<DK, DV, NB>(t2, r2, last_row, k, lane, sh_q, m_run, l_run, acc);
+          t += 3;
+        } else {
+          const int r0 = row_of(t, c, cn);
+          const int r1 = row_of(t + 1, c, cn);
+          load_tile(t1, Ks, Vs, r1, last_row, i, k);
+          if (r0 <= last_row)
+            process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
+          load_tile(t0, Ks, Vs, row_of(t + 2, c, cn), last_row, i, k);
+          if (r1 <= last_row)
+            process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
+          t += 2;
+        }
       } while (t < tpw);
       if (tid == 0) sh_next[it & 1] = after;
       __syncthreads();
@@ -459,8 +493,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     // Row sums of head i are spread over the 4 row groups k.
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      l_run[nb] += __shfl_xor(l_run[nb], 16);
-      l_run[nb] += __shfl_xor(l_run[nb], 32);
+      l_run[nb] = sum_over_row_groups(l_run[nb]);
     }
 
     // Combine the 4 waves: waves 1..3 park their state in LDS in their own
@@ -642,7 +675,8 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int64_t chunks_per_slab = ceil_div(n_max, chunk_rows);
   // One resident workgroup per CU and wave slot, fewer if there are fewer
   // chunks than that.
-  const int64_t resident = (int64_t)kComputeUnits;
+  const int64_t resident = (int64_t)kComputeUnits * (plan->blocks == 1 ? kWavesPerSimd<1>
+                                                                        : kWavesPerSimd<2>);
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
   // A slab is visited at most once per workgroup and per chunk; kVisitSlack
   // times the even share of workgroups per slab leaves room for workgroups

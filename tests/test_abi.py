@@ -50,7 +50,7 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     groups = -(-G // 32)
     slabs = B * h_kv * groups
     chunks = -(-n_max // c)
-    resident = 256
+    resident = 256 * (1 if G <= 16 else 2)
     grid = max(1, min(resident, chunks * slabs))
     J = max(1, min(chunks, 4 * -(-grid // slabs)))
     slots = B * h_q * J
@@ -63,14 +63,14 @@ def test_chunk_rows_and_workspace_sizes():
                  (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
                  (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]:
         c = binding.chunk_rows(*args)
-        assert c >= 192 and c % 192 == 0
+        assert c >= 384 and c % 384 == 0
         counters, total = _expected_workspace(*args, c)
         assert binding.workspace_counter_bytes(*args) == counters
         assert binding.workspace_bytes(*args) == total
-        assert binding.workspace_bytes(*args, 192) == _expected_workspace(*args, 192)[1]
+        assert binding.workspace_bytes(*args, 384) == _expected_workspace(*args, 384)[1]
     assert binding.chunk_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
     assert binding.workspace_bytes(1, 1, 1, 10, 96, 64) == 0  # unsupported d_k
-    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 128) == 0  # chunk not a multiple of 192
+    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 192) == 0  # chunk not a multiple of 384
 
 
 def _decode(**kw):
@@ -88,7 +88,7 @@ def _decode(**kw):
     (dict(out=None), 1),
     (dict(B=0), 2), (dict(h_q=0), 2), (dict(h_kv=0), 2), (dict(n_max=0), 2),
     (dict(h_q=3, h_kv=2), 2), (dict(B=1 << 21), 2), (dict(chunk=100), 2),
-    (dict(chunk=128), 2), (dict(chunk=-192), 2),
+    (dict(chunk=192), 2), (dict(chunk=-384), 2),
     (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=256), 3),
     (dict(q=FAKE + 4), 4), (dict(K=FAKE + 8), 4), (dict(out=FAKE + 4), 4),
     (dict(len=FAKE + 2), 4),
