@@ -3,7 +3,8 @@
 
 One step = one pass of the whole path over one batch: KV append (every KV
 head of every sequence gets one new row) followed by decode attention of
-every query head (partials, then the merge).  The default workload is
+every query head -- run as the fused step, two kernels: the partial kernel
+(which also performs the append) and the merge (which also advances len).  The default workload is
 the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
 len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
 
@@ -186,18 +187,23 @@ def main() -> int:
     torch.cuda.synchronize()
 
     def step(i, ev_a=None, ev_b=None):
+        # One step: the append fused into the decode's partial kernel, then
+        # the merge (which also advances len) -- da_decode_step, with the
+        # partial kernel bracketed by events.
         t = i % nsteps_in
-        if s.steps:
-            if t == 0 and i > 0:
-                dl.copy_(lens0)          # a new pass over the 64-step sequence
-            binding.kv_append(dK, dV, dkn[t], dvn[t], dl, stream=stream)
+        if s.steps and t == 0 and i > 0:
+            dl.copy_(lens0)              # a new pass over the 64-step sequence
         if ev_a is not None:
             ev_a.record(stream)
-        binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=stream)
+        if s.steps:
+            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk,
+                                   k_new=dkn[t], v_new=dvn[t], stream=stream)
+        else:
+            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=stream)
         if ev_b is not None:
             ev_b.record(stream)
         binding.decode_merge(out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
-                             chunk, stream=stream)
+                             chunk, lens=dl if s.steps else None, stream=stream)
 
     log(f"warmup {args.warmup} step(s), chunk_rows={chunk}")
     for i in range(args.warmup):
@@ -240,7 +246,9 @@ def main() -> int:
         return b
 
     alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
-    partial_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v)
+    # The partial kernel of a step also writes the appended rows (Prop. 2).
+    append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v) if s.steps else 0
+    partial_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
                      for l in step_lens]
     ms_per_step = total_ms / args.steps
     value = alg_bytes / (total_ms * 1e-3) / 1e9
@@ -267,7 +275,7 @@ def main() -> int:
             "initial_len": [int(x) for x in inp.lens],
             "steps_per_sequence": s.steps,
             "chunk_rows": chunk,
-            "step": "kv_append + decode_partial + decode_merge" if s.steps
+            "step": "decode_partial with fused kv_append + decode_merge" if s.steps
                     else "decode_partial + decode_merge",
         },
         "us_per_step": round(ms_per_step * 1e3, 2),

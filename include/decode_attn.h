@@ -133,28 +133,50 @@ da_status da_decode_attn(const float *q, const float *K, const float *V,
                          size_t workspace_bytes, void *stream);
 
 /*
- * First half of da_decode_attn: scores of all G query heads of each group
- * over the slab's rows (K and V rows read from HBM once per (b, KV head)),
- * their running maxima, sums of exponentials and unnormalised weighted sums
- * of V rows, written to the workspace as per-visit partials.  Must be
- * followed by da_decode_merge on the same workspace (which also re-zeroes the
- * counters).  Arguments as for da_decode_attn (no `out`).
+ * Append and decode in one step: the effect of da_kv_append(K, V, k_new,
+ * v_new, len, ...) followed by da_decode_attn(q, K, V, len, ...) -- eqs.
+ * (6)-(7) then (1)-(3), the order of one autoregressive step of the paper's
+ * multi-step cache -- in two kernel launches instead of three: the decode
+ * reads the new row of each KV head straight from k_new / v_new (and writes
+ * it into the cache meanwhile), and the merge advances len.  Same results,
+ * same argument rules as the two calls; k_new [B][h_kv][d_k] and
+ * v_new [B][h_kv][d_v] must not overlap K / V.
  */
-da_status da_decode_partial(const float *q, const float *K, const float *V,
+da_status da_decode_step(const float *q, float *K, float *V,
+                         const float *k_new, const float *v_new, int32_t *len,
+                         float scale, float *out, int B, int h_q, int h_kv,
+                         int n_max, int d_k, int d_v, int chunk_rows,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * First half of da_decode_attn / da_decode_step: scores of all G query heads
+ * of each group over the slab's rows (K and V rows read from HBM once per
+ * (b, KV head)), their running maxima, sums of exponentials and unnormalised
+ * weighted sums of V rows, written to the workspace as per-visit partials.
+ * k_new and v_new are both NULL (plain decode; K and V are only read) or both
+ * set (the fused append of da_decode_step: row len[b] of every KV head is
+ * taken from them and written into K / V).  Must be followed by
+ * da_decode_merge on the same workspace, which also re-zeroes the counters.
+ */
+da_status da_decode_partial(const float *q, float *K, float *V,
+                            const float *k_new, const float *v_new,
                             const int32_t *len, float scale, int B, int h_q,
                             int h_kv, int n_max, int d_k, int d_v,
                             int chunk_rows, void *workspace,
                             size_t workspace_bytes, void *stream);
 
 /*
- * Second half of da_decode_attn: combines the partials of every (b, query
- * head) into out[b,h,:] (running maximum, rescaled sums, one division) and
- * resets the workspace counters to zero.  chunk_rows and the shapes must be
- * those of the da_decode_partial call that filled the workspace.
+ * Second half: combines the partials of every (b, query head) into
+ * out[b,h,:] (running maximum, rescaled sums, one division) and resets the
+ * workspace counters to zero.  chunk_rows and the shapes must be those of the
+ * da_decode_partial call that filled the workspace.  len is NULL after a
+ * plain decode; after a partial with a fused append it is that call's len,
+ * and every len[b] with 0 <= len[b] < n_max advances by one.
  */
-da_status da_decode_merge(float *out, int B, int h_q, int h_kv, int n_max,
-                          int d_k, int d_v, int chunk_rows, void *workspace,
-                          size_t workspace_bytes, void *stream);
+da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
+                          int n_max, int d_k, int d_v, int chunk_rows,
+                          void *workspace, size_t workspace_bytes,
+                          void *stream);
 
 /*
  * KV-cache append, eqs. (6)-(7) (K_{t+1} = K_t # k_t, V_{t+1} = V_t # v_t,

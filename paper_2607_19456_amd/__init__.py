@@ -11,7 +11,7 @@ built library; using the decode or append without it raises ImportError.
 from importlib import import_module
 
 _BINDING_NAMES = {
-    "decode_attn", "decode_partial", "decode_merge", "kv_append",
+    "decode_attn", "decode_step", "decode_partial", "decode_merge", "kv_append",
     "chunk_rows", "workspace_bytes", "workspace_counter_bytes", "alloc_workspace", "DecodeAttnError",
     "LIBRARY_PATH",
 }

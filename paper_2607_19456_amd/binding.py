@@ -31,8 +31,9 @@ SIGNATURES = {
     "da_decode_workspace_bytes": (_sz, [_ci] * 7),
     "da_decode_workspace_counter_bytes": (_sz, [_ci] * 6),
     "da_decode_attn": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_partial": (_ci, [_vp, _vp, _vp, _vp, _cf] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_merge": (_ci, [_vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_partial": (_ci, [_vp] * 6 + [_cf] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
 }
 
@@ -142,25 +143,58 @@ def decode_attn(q, K, V, lens, scale: float, out=None, workspace=None,
     return out
 
 
+def decode_step(q, K, V, k_new, v_new, lens, scale: float, out=None, workspace=None,
+                chunk_rows: int = 0, stream=None) -> torch.Tensor:
+    """kv_append(K, V, k_new, v_new, lens) then decode_attn(q, K, V, lens),
+    fused into two kernel launches."""
+    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
+    if out is None:
+        out = torch.empty((B, h_q, d_v), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(q, K, V, chunk_rows)
+    wp, wn = _ws(workspace)
+    _check("da_decode_step", _lib.da_decode_step(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(k_new, "k_new", torch.float32),
+        _dev(v_new, "v_new", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
+        d_v, int(chunk_rows), wp, wn, _stream(stream)))
+    return out
+
+
+def _new_rows(k_new, v_new, B, h_kv, d_k, d_v):
+    if tuple(k_new.shape) != (B, h_kv, d_k) or tuple(v_new.shape) != (B, h_kv, d_v):
+        raise ValueError("k_new must be [B,h_kv,d_k] and v_new [B,h_kv,d_v]")
+
+
 def decode_partial(q, K, V, lens, scale: float, workspace, chunk_rows: int = 0,
-                   stream=None) -> None:
-    """Partials of the decode into ``workspace`` (follow with decode_merge)."""
+                   k_new=None, v_new=None, stream=None) -> None:
+    """Partials of the decode into ``workspace`` (follow with decode_merge).
+    With ``k_new``/``v_new`` the partial also performs the fused append."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     wp, wn = _ws(workspace)
+    kp = vp = None
+    if k_new is not None or v_new is not None:
+        _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
+        kp = _dev(k_new, "k_new", torch.float32)
+        vp = _dev(v_new, "v_new", torch.float32)
     _check("da_decode_partial", _lib.da_decode_partial(
         _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
-        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+        _dev(V, "V", torch.float32), kp, vp, _dev(lens, "len", torch.int32),
         float(scale), B, h_q, h_kv, n_max, d_k, d_v, int(chunk_rows), wp, wn,
         _stream(stream)))
 
 
 def decode_merge(out, workspace, B, h_q, h_kv, n_max, d_k, d_v,
-                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
+                 chunk_rows: int = 0, lens=None, stream=None) -> torch.Tensor:
     """Combine the partials in ``workspace`` into ``out`` (re-zeroes the
-    workspace counters)."""
+    workspace counters).  ``lens``: after a partial with a fused append, the
+    lengths to advance by one."""
     wp, wn = _ws(workspace)
+    lp = None if lens is None else _dev(lens, "len", torch.int32)
     _check("da_decode_merge", _lib.da_decode_merge(
-        _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k, d_v,
+        _dev(out, "out", torch.float32), lp, B, h_q, h_kv, n_max, d_k, d_v,
         int(chunk_rows), wp, wn, _stream(stream)))
     return out
 
@@ -173,8 +207,7 @@ def kv_append(K, V, k_new, v_new, lens, stream=None) -> None:
     d_v = V.shape[3]
     if tuple(V.shape[:3]) != (B, h_kv, n_max):
         raise ValueError("K and V disagree in [B,h_kv,n_max]")
-    if tuple(k_new.shape) != (B, h_kv, d_k) or tuple(v_new.shape) != (B, h_kv, d_v):
-        raise ValueError("k_new must be [B,h_kv,d_k] and v_new [B,h_kv,d_v]")
+    _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
     _check("da_kv_append", _lib.da_kv_append(
         _dev(K, "K", torch.float32), _dev(V, "V", torch.float32),
         _dev(k_new, "k_new", torch.float32), _dev(v_new, "v_new", torch.float32),

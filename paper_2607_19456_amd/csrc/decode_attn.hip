@@ -52,17 +52,16 @@ constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
 constexpr int kResidentWorkgroups = kComputeUnits * 2;  // upper bound of the resident set
 // Register tiles per wave in the load ring, and waves per SIMD, of the
-// partial kernel.  One MFMA column block (<= 16 heads): a three-tile ring at
-// one wave per SIMD keeps two tiles' loads in flight during each tile's
-// products.  Two column blocks (17..32 heads) double the matrix work per
-// tile: a two-tile ring leaves room for two waves per SIMD, so one wave's
-// products overlap the other's loads.
+// partial kernel: a three-tile ring at one wave per SIMD keeps two tiles'
+// loads in flight during each tile's products.  (Measured alternatives: two
+// tiles at two waves per SIMD is slower both for groups of <= 16 heads and
+// for groups of 17..32, whose two column blocks double the matrix work.)
 template <int NB>
 constexpr int kRing = 3;
 template <int NB>
 constexpr int kWavesPerSimd = 1;
 // A chunk is the rows a workgroup takes at a time: a multiple of six 16-row
-// tiles per wave (whole turns of either ring).
+// tiles per wave (whole turns of the three-tile ring).
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 constexpr int kDefaultChunkRows = 768;
 // Visit slots per slab, in units of the even share of waves per slab.
@@ -118,6 +117,16 @@ __device__ __forceinline__ int rows_used(int32_t len_b, int n_max) {
   return len_b < 0 ? 0 : (len_b > n_max ? n_max : len_b);
 }
 
+// With a fused append, the decode of sequence b also covers row len[b] (the
+// appended one) when the cache has room for it.
+__device__ __forceinline__ bool appends(bool app, int32_t len_b, int n_max) {
+  return app && len_b >= 0 && len_b < n_max;
+}
+
+__device__ __forceinline__ int decode_rows(int32_t len_b, int n_max, bool app) {
+  return appends(app, len_b, n_max) ? len_b + 1 : rows_used(len_b, n_max);
+}
+
 // ---------------------------------------------------------------------------
 // KV append.  One workgroup per sequence; every thread reads len[b] before
 // the barrier, thread 0 writes it after, so no thread can see the new value.
@@ -164,21 +173,29 @@ struct Tile {
   f4 v[4][DV / 64];       // V rows: lane (i,k) holds row 4k+rho, dims 64c+4i..+3
 };
 
+// Where a tile's rows live: the slab, except row `new_row` (the row a fused
+// append adds; -1 if none), which is read from the incoming k_new / v_new rows.
+struct RowSource {
+  const float* __restrict__ Ks;
+  const float* __restrict__ Vs;
+  const float* __restrict__ k_new_row;
+  const float* __restrict__ v_new_row;
+  int new_row;
+};
+
 template <int DK, int DV, int NB>
-__device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T,
-                                          const float* __restrict__ Ks,
-                                          const float* __restrict__ Vs,
+__device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& src,
                                           int row0, int last_row, int i, int k) {
   const int rk = min(row0 + i, last_row);
+  const float* kp = rk == src.new_row ? src.k_new_row : src.Ks + (int64_t)rk * DK;
 #pragma unroll
-  for (int t = 0; t < DK / 16; ++t)
-    T.k[t] = load4_stream(Ks + (int64_t)rk * DK + 16 * t + 4 * k);
+  for (int t = 0; t < DK / 16; ++t) T.k[t] = load4_stream(kp + 16 * t + 4 * k);
 #pragma unroll
   for (int rho = 0; rho < 4; ++rho) {
     const int rv = min(row0 + 4 * k + rho, last_row);
+    const float* vp = rv == src.new_row ? src.v_new_row : src.Vs + (int64_t)rv * DV;
 #pragma unroll
-    for (int c = 0; c < DV / 64; ++c)
-      T.v[rho][c] = load4_stream(Vs + (int64_t)rv * DV + 64 * c + 4 * i);
+    for (int c = 0; c < DV / 64; ++c) T.v[rho][c] = load4_stream(vp + 64 * c + 4 * i);
   }
 }
 
@@ -254,8 +271,8 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
 
 // Number of cache rows of slab s = (b, KV head, head group).
 __device__ __forceinline__ int slab_rows(const int32_t* __restrict__ len, int s, int per_b,
-                                         int n_max) {
-  return rows_used(len[s / per_b], n_max);
+                                         int n_max, bool app) {
+  return decode_rows(len[s / per_b], n_max, app);
 }
 
 __device__ __forceinline__ unsigned load_counter(const unsigned* p) {
@@ -268,14 +285,15 @@ __device__ __forceinline__ unsigned load_counter(const unsigned* p) {
 // slabs examined up to and including the one returned.
 __device__ int find_open_slab(const unsigned* __restrict__ cnt,
                               const int32_t* __restrict__ len, int start, int budget, int S,
-                              int per_b, int n_max, int C, int J, int lane, int* seen) {
+                              int per_b, int n_max, bool app, int C, int J, int lane,
+                              int* seen) {
   for (int base = 0; base < budget; base += kWave) {
     const int o = base + lane;
     int sl = start + o;
     if (sl >= S) sl -= S;
     bool open = false;
     if (o < budget) {
-      const int nch = (slab_rows(len, sl, per_b, n_max) + C - 1) / C;
+      const int nch = (slab_rows(len, sl, per_b, n_max, app) + C - 1) / C;
       const unsigned* c = cnt + (size_t)sl * kCounterStride;
       open = (int)load_counter(c + kCtr) < nch && (int)load_counter(c + kVis) < J;
     }
@@ -314,14 +332,16 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB>
 __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_kernel(
-    const float* __restrict__ q, const float* __restrict__ K,
-    const float* __restrict__ V, const int32_t* __restrict__ len,
+    const float* __restrict__ q, float* __restrict__ K,
+    float* __restrict__ V, const float* __restrict__ k_new,
+    const float* __restrict__ v_new, const int32_t* __restrict__ len,
     float qscale, int B, int h_q, int h_kv, int n_max, int C, int head_groups, int J,
     unsigned* __restrict__ cnt, float2* __restrict__ ws_ml, float* __restrict__ ws_acc) {
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
-  const int tpw = C / (kTileRows * kWaves);             // tiles per wave per chunk (even)
+  const int tpw = C / (kTileRows * kWaves);             // tiles per wave per chunk
+  const bool app = k_new != nullptr;                    // fused append (eqs. (6)-(7))
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -336,6 +356,28 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
   __shared__ float sh_m[kWaves - 1][NB][kWave];
   __shared__ float sh_l[kWaves - 1][NB][kWave];
 
+  // Fused append: the workgroups share the row copies -- row len[b] of every
+  // KV head <- k_new / v_new, bit for bit.  The decode below never reads
+  // that row from the cache (it takes it straight from k_new / v_new), so no
+  // ordering between the copies and the reads is needed; len[b] itself is
+  // only advanced by the merge, after every workgroup has read it.
+  if (app) {
+    constexpr int ck = DK / 4, cv = DV / 4;             // 16-byte chunks per row
+    for (int u = blockIdx.x; u < B * h_kv; u += gridDim.x) {
+      const int b = u / h_kv;
+      const int32_t t = len[b];
+      if (t < 0 || t >= n_max) continue;
+      const int64_t row = (int64_t)u * n_max + t;
+      for (int w = tid; w < ck + cv; w += kThreads) {
+        if (w < ck)
+          reinterpret_cast<u4*>(K + row * DK)[w] = reinterpret_cast<const u4*>(k_new + (int64_t)u * DK)[w];
+        else
+          reinterpret_cast<u4*>(V + row * DV)[w - ck] =
+              reinterpret_cast<const u4*>(v_new + (int64_t)u * DV)[w - ck];
+      }
+    }
+  }
+
   int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
 
   while (true) {
@@ -346,12 +388,12 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       int budget = S;
       while (budget > 0) {
         int seen;
-        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, C, J, lane,
-                                        &seen);
+        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, C, J,
+                                        lane, &seen);
         if (cand < 0) break;
         budget -= seen;
         start = cand + 1 == S ? 0 : cand + 1;
-        const int nch = (slab_rows(len, cand, per_b, n_max) + C - 1) / C;
+        const int nch = (slab_rows(len, cand, per_b, n_max, app) + C - 1) / C;
         int slot = -1, got = -1, nxt = -1;
         if (lane == 0) {
           unsigned* cc = cnt + (size_t)cand * kCounterStride;
@@ -393,14 +435,19 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     const int rem = s - b * per_b;
     const int g = rem / head_groups;
     const int hgrp = rem - g * head_groups;
-    const int n = slab_rows(len, s, per_b, n_max);
+    const int32_t len_b = len[b];
+    const int n = decode_rows(len_b, n_max, app);
     const int nch = (n + C - 1) / C;
     const int last_row = n - 1;
     const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
     const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
     const int64_t slab = (int64_t)b * h_kv + g;
-    const float* __restrict__ Ks = K + slab * n_max * DK;
-    const float* __restrict__ Vs = V + slab * n_max * DV;
+    RowSource src;
+    src.Ks = K + slab * n_max * DK;
+    src.Vs = V + slab * n_max * DV;
+    src.new_row = appends(app, len_b, n_max) ? len_b : -1;
+    src.k_new_row = app ? k_new + slab * DK : nullptr;
+    src.v_new_row = app ? v_new + slab * DV : nullptr;
 
     // B operand of the score product, staged in LDS in register order: entry
     // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
@@ -443,8 +490,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
                                   : last_row);
     };
     Tile<DK, DV, NB> t0, t1, t2;
-    load_tile(t0, Ks, Vs, row_of(0, c, cn), last_row, i, k);
-    if constexpr (kRing<NB> == 3) load_tile(t1, Ks, Vs, row_of(1, c, cn), last_row, i, k);
+    load_tile(t0, src, row_of(0, c, cn), last_row, i, k);
+    if constexpr (kRing<NB> == 3) load_tile(t1, src, row_of(1, c, cn), last_row, i, k);
     for (int it = 0;; ++it) {
       // Thread 0 asks for the chunk after next even on the last chunk (the
       // counter simply runs past the end): a conditional request would merge
@@ -461,23 +508,23 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
           const int r0 = row_of(t, c, cn);
           const int r1 = row_of(t + 1, c, cn);
           const int r2 = row_of(t + 2, c, cn);
-          load_tile(t2, Ks, Vs, r2, last_row, i, k);
+          load_tile(t2, src, r2, last_row, i, k);
           if (r0 <= last_row)
             process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t0, Ks, Vs, row_of(t + 3, c, cn), last_row, i, k);
+          load_tile(t0, src, row_of(t + 3, c, cn), last_row, i, k);
           if (r1 <= last_row)
             process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t1, Ks, Vs, row_of(t + 4, c, cn), last_row, i, k);
+          load_tile(t1, src, row_of(t + 4, c, cn), last_row, i, k);
           if (r2 <= last_row)
             process_tile<DK, DV, NB>(t2, r2, last_row, k, lane, sh_q, m_run, l_run, acc);
           t += 3;
         } else {
           const int r0 = row_of(t, c, cn);
           const int r1 = row_of(t + 1, c, cn);
-          load_tile(t1, Ks, Vs, r1, last_row, i, k);
+          load_tile(t1, src, r1, last_row, i, k);
           if (r0 <= last_row)
             process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t0, Ks, Vs, row_of(t + 2, c, cn), last_row, i, k);
+          load_tile(t0, src, row_of(t + 2, c, cn), last_row, i, k);
           if (r1 <= last_row)
             process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
           t += 2;
@@ -566,7 +613,8 @@ template <int DV>
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
     float* __restrict__ out, const float2* __restrict__ ws_ml,
     const float* __restrict__ ws_acc, int h_q, int h_kv, int head_groups, int heads_per_group,
-    int merge_heads, int J, unsigned* __restrict__ cnt) {
+    int merge_heads, int J, unsigned* __restrict__ cnt, int32_t* __restrict__ len_bump,
+    int n_max) {
   constexpr int kChunks = DV / 4;                       // 16-byte columns per row
   constexpr int kLanesV = kThreads / kChunks;           // visits merged in parallel
   const int s = blockIdx.x / merge_heads;
@@ -579,6 +627,12 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
   const int G = h_q / h_kv;
   const int h_count = min(heads_per_group, G - hgrp * heads_per_group);
   if (hl >= h_count) return;                            // padding workgroup
+  // Completing a fused append: len[b] advances once per sequence, after the
+  // partial kernel (which read it) has finished.
+  if (len_bump && g == 0 && hgrp == 0 && hl == 0 && threadIdx.x == 0) {
+    const int32_t t = len_bump[b];
+    if (t >= 0 && t < n_max) len_bump[b] = t + 1;
+  }
   unsigned* slab_cnt = cnt + (size_t)s * kCounterStride;
   const int nv = min((int)slab_cnt[kVis], J);
   const int ch = threadIdx.x % kChunks;
@@ -709,34 +763,43 @@ da_status launch_status() {
   return hipGetLastError() == hipSuccess ? DA_OK : DA_ERR_HIP;
 }
 
+struct PartialArgs {
+  const float* q;
+  float* K;
+  float* V;
+  const float* k_new;   // both NULL: plain decode; both set: fused append
+  const float* v_new;
+  const int32_t* len;
+  float qscale;
+  int B, h_q, h_kv, n_max;
+};
+
 template <int DK, int DV, int NB>
-void launch_partial(const Plan& pl, const float* q, const float* K, const float* V,
-                    const int32_t* len, float qscale, int B, int h_q, int h_kv, int n_max,
-                    const WsView& w, hipStream_t stream) {
+void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
   hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB>), dim3(pl.grid), dim3(kThreads), 0,
-                     stream, q, K, V, len, qscale, B, h_q, h_kv, n_max, pl.chunk_rows,
-                     pl.head_groups, pl.J, w.cnt, w.ml, w.acc);
+                     stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
+                     a.h_kv, a.n_max, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.ml, w.acc);
 }
 
 template <int DK, int DV>
-void launch_partial_nb(const Plan& pl, const float* q, const float* K, const float* V,
-                       const int32_t* len, float qscale, int B, int h_q, int h_kv,
-                       int n_max, const WsView& w, hipStream_t s) {
+void launch_partial_nb(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t s) {
   if (pl.blocks == 1)
-    launch_partial<DK, DV, 1>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+    launch_partial<DK, DV, 1>(pl, a, w, s);
   else
-    launch_partial<DK, DV, 2>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+    launch_partial<DK, DV, 2>(pl, a, w, s);
 }
 
-da_status partial_impl(const float* q, const float* K, const float* V, const int32_t* len,
-                       float scale, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                       int chunk_rows, void* workspace, size_t workspace_bytes,
-                       void* stream, Plan* out_plan) {
+da_status partial_impl(const float* q, const float* K, const float* V, const float* k_new,
+                       const float* v_new, const int32_t* len, float scale, int B, int h_q,
+                       int h_kv, int n_max, int d_k, int d_v, int chunk_rows, void* workspace,
+                       size_t workspace_bytes, void* stream, Plan* out_plan) {
   if (!q || !K || !V || !len) return DA_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return DA_ERR_NULL;
   Plan pl;
   da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
-  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4))
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4) ||
+      !aligned(k_new, 16) || !aligned(v_new, 16))
     return DA_ERR_ALIGN;
   if (!std::isfinite(scale)) return DA_ERR_SCALE;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
@@ -744,23 +807,26 @@ da_status partial_impl(const float* q, const float* K, const float* V, const int
   if (out_plan) *out_plan = pl;
 
   const WsView w = view(pl, workspace);
-  const float qscale = scale * kLog2e;
+  // K and V are written only when a fused append is asked for (k_new set).
+  const PartialArgs a{q, const_cast<float*>(K), const_cast<float*>(V), k_new, v_new, len,
+                      scale * kLog2e, B, h_q, h_kv, n_max};
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
-  else if (d_k == 64 && d_v == 128) launch_partial_nb<64, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
-  else if (d_k == 128 && d_v == 64) launch_partial_nb<128, 64>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
-  else launch_partial_nb<128, 128>(pl, q, K, V, len, qscale, B, h_q, h_kv, n_max, w, s);
+  if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, a, w, s);
+  else if (d_k == 64 && d_v == 128) launch_partial_nb<64, 128>(pl, a, w, s);
+  else if (d_k == 128 && d_v == 64) launch_partial_nb<128, 64>(pl, a, w, s);
+  else launch_partial_nb<128, 128>(pl, a, w, s);
   return launch_status();
 }
 
-da_status merge_impl(float* out, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                     int chunk_rows, void* workspace, size_t workspace_bytes, void* stream) {
+da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, int n_max,
+                     int d_k, int d_v, int chunk_rows, void* workspace, size_t workspace_bytes,
+                     void* stream) {
   if (!out) return DA_ERR_NULL;
   Plan pl;
   da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
-  if (!aligned(out, 16)) return DA_ERR_ALIGN;
+  if (!aligned(out, 16) || !aligned(len_bump, 4)) return DA_ERR_ALIGN;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
 
@@ -771,10 +837,12 @@ da_status merge_impl(float* out, int B, int h_q, int h_kv, int n_max, int d_k, i
   const dim3 grid((unsigned)pl.slabs * (unsigned)pl.merge_heads);
   if (d_v == 64)
     hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
-                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt);
+                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
+                       len_bump, n_max);
   else
     hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
-                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt);
+                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
+                       len_bump, n_max);
   return launch_status();
 }
 
@@ -816,18 +884,18 @@ size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max, in
   return pl.counter_bytes;
 }
 
-da_status da_decode_partial(const float* q, const float* K, const float* V,
-                            const int32_t* len, float scale, int B, int h_q, int h_kv,
-                            int n_max, int d_k, int d_v, int chunk_rows, void* workspace,
-                            size_t workspace_bytes, void* stream) {
-  return partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
-                      workspace, workspace_bytes, stream, nullptr);
+da_status da_decode_partial(const float* q, float* K, float* V, const float* k_new,
+                            const float* v_new, const int32_t* len, float scale, int B,
+                            int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
+                      chunk_rows, workspace, workspace_bytes, stream, nullptr);
 }
 
-da_status da_decode_merge(float* out, int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                          int chunk_rows, void* workspace, size_t workspace_bytes,
-                          void* stream) {
-  return merge_impl(out, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, workspace,
+da_status da_decode_merge(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
+                          int d_k, int d_v, int chunk_rows, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 
@@ -844,10 +912,29 @@ da_status da_decode_attn(const float* q, const float* K, const float* V, const i
     return st != DA_OK ? st : DA_ERR_ALIGN;
   }
   Plan pl;
-  da_status st = partial_impl(q, K, V, len, scale, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
-                              workspace, workspace_bytes, stream, &pl);
+  da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
+                              d_v, chunk_rows, workspace, workspace_bytes, stream, &pl);
   if (st != DA_OK) return st;
-  return merge_impl(out, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
+  return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
+                    workspace_bytes, stream);
+}
+
+da_status da_decode_step(const float* q, float* K, float* V, const float* k_new,
+                         const float* v_new, int32_t* len, float scale, float* out, int B,
+                         int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!out || !k_new || !v_new) return DA_ERR_NULL;
+  if (!aligned(out, 16)) {
+    if (!q || !K || !V || !len) return DA_ERR_NULL;
+    Plan pl;
+    da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
+    return st != DA_OK ? st : DA_ERR_ALIGN;
+  }
+  Plan pl;
+  da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
+                              chunk_rows, workspace, workspace_bytes, stream, &pl);
+  if (st != DA_OK) return st;
+  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 

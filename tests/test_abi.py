@@ -50,7 +50,7 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     groups = -(-G // 32)
     slabs = B * h_kv * groups
     chunks = -(-n_max // c)
-    resident = 256 * (1 if G <= 16 else 2)
+    resident = 256
     grid = max(1, min(resident, chunks * slabs))
     J = max(1, min(chunks, 4 * -(-grid // slabs)))
     slots = B * h_q * J
@@ -100,21 +100,35 @@ def test_decode_validation(kw, status):
     assert _decode(**kw) == status
 
 
-def test_partial_and_merge_validation():
-    p = lib.da_decode_partial(None, FAKE, FAKE, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
-                              FAKE, 1 << 20, None)
-    assert p == 1
-    p = lib.da_decode_partial(FAKE, FAKE, FAKE, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
-                              FAKE, 8, None)
-    assert p == 6
-    m = lib.da_decode_merge(None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
-    assert m == 1
-    m = lib.da_decode_merge(FAKE, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None)
-    assert m == 2
-    m = lib.da_decode_merge(FAKE, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None)
-    assert m == 6
-    m = lib.da_decode_merge(FAKE + 4, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None)
-    assert m == 4
+def test_partial_merge_and_step_validation():
+    P = lib.da_decode_partial
+    assert P(None, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+             FAKE, 1 << 20, None) == 1
+    assert P(FAKE, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+             FAKE, 8, None) == 6
+    # k_new and v_new come together or not at all
+    assert P(FAKE, FAKE, FAKE, FAKE, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+             FAKE, 1 << 20, None) == 1
+    assert P(FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+             FAKE, 1 << 20, None) == 4
+    M = lib.da_decode_merge
+    assert M(None, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 1
+    assert M(FAKE, None, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None) == 2
+    assert M(FAKE, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None) == 6
+    assert M(FAKE + 4, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
+    assert M(FAKE, FAKE + 2, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
+    S = lib.da_decode_step
+    args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 1, 1, 64, 64, 64, 0,
+            FAKE, 1 << 20, None]
+    for pos in (0, 1, 2, 3, 4, 5, 7):
+        a = list(args); a[pos] = None
+        assert S(*a) == 1, pos
+    a = list(args); a[7] = FAKE + 4
+    assert S(*a) == 4
+    a = list(args); a[16] = 8
+    assert S(*a) == 6
+    a = list(args); a[6] = float("nan")
+    assert S(*a) == 5
 
 
 @pytest.mark.parametrize("args,status", [

@@ -165,6 +165,8 @@ def test_decode_partial_then_merge_equals_decode(cuda_device):
     binding.decode_partial(dq, dK, dV, dl, float(shape.scale32()), ws)
     binding.decode_merge(out, ws, 2, 16, 2, 900, 128, 128)
     torch.cuda.synchronize()
+    assert dl.cpu().numpy().tolist() == [900, 450]   # a plain decode leaves len alone
+    torch.cuda.synchronize()
     ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
     check(out.cpu().numpy().astype(np.float64), ref, "partial+merge")
 
@@ -178,6 +180,62 @@ def test_validation_errors_raise(cuda_device):
         binding.decode_attn(dq, dK, dV, dl, 0.1, workspace=small)
     with pytest.raises(binding.DecodeAttnError, match="SCALE"):
         binding.decode_attn(dq, dK, dV, dl, float("nan"))
+
+
+# --- fused append + decode step ------------------------------------------------
+
+STEP_CASES = [
+    # name, B, h_q, h_kv, d_k, d_v, n_max, lens (initial)
+    ("gqa8", 3, 16, 2, 128, 128, 700, [0, 333, 699]),     # empty, middle, fills up
+    ("mha_d64", 2, 4, 4, 64, 64, 300, [299, 300]),         # one full cache: no append
+    ("mqa32_dkdv", 2, 32, 1, 64, 128, 200, [5, 190]),
+    ("neg_len", 2, 8, 4, 128, 128, 100, [-3, 40]),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES, ids=[c[0] for c in STEP_CASES])
+def test_fused_step_equals_append_then_decode(cuda_device, case):
+    name, B, h_q, h_kv, d_k, d_v, n_max, lens = case
+    shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v,
+                             n_max=n_max, steps=3)
+    inp = workloads.make(shape, seed=zlib.crc32(name.encode()) % 1000,
+                         lens=np.array(lens, np.int32))
+    dK, dV, dl = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    hK, hV, hl = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    ws = poisoned_workspace(dev(inp.q, cuda_device), dK, dV)
+    for t in range(shape.steps):
+        say(f"step {name} t={t} len={hl.tolist()}")
+        out = binding.decode_step(dev(inp.q_step[t], cuda_device), dK, dV,
+                                  dev(inp.k_new[t], cuda_device), dev(inp.v_new[t], cuda_device),
+                                  dl, float(shape.scale32()), workspace=ws)
+        torch.cuda.synchronize()
+        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+        ref = oracle.decode(inp.q_step[t], hK, hV, hl, shape.scale32())
+        assert dl.cpu().numpy().tolist() == hl.tolist()
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))
+        assert np.array_equal(dV.cpu().numpy().view(np.uint32), hV.view(np.uint32))
+        check(out.cpu().numpy().astype(np.float64), ref, f"step {name} t={t}")
+
+
+def test_fused_step_long_context_sampled(cuda_device):
+    """The long-context workload's first steps through the fused path, checked
+    on sampled heads (the oracle replays the appends on the host)."""
+    shape = workloads.get("c5")
+    say("fused step long-context: generating inputs")
+    inp = workloads.make(shape, seed=3)
+    dK, dV, dl = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    hK, hV, hl = inp.K, inp.V, inp.lens.copy()
+    ws = binding.alloc_workspace(dev(inp.q, cuda_device), dK, dV)
+    for t in range(4):
+        out = binding.decode_step(dev(inp.q_step[t], cuda_device), dK, dV,
+                                  dev(inp.k_new[t], cuda_device), dev(inp.v_new[t], cuda_device),
+                                  dl, float(shape.scale32()), workspace=ws)
+        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+        torch.cuda.synchronize()
+        heads = _sample_heads(shape.B, shape.h_q, 2, 100 + t)
+        ref = oracle.decode(inp.q_step[t], hK, hV, hl, shape.scale32(), heads=heads)
+        check(out.cpu().numpy().astype(np.float64)[heads], ref[heads], f"fused step {t}")
+        assert dl.cpu().numpy().tolist() == hl.tolist()
 
 
 # --- append: bit-exact --------------------------------------------------------
