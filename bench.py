@@ -4,7 +4,9 @@
 One step = one pass of the whole path over one batch: KV append (every KV
 head of every sequence gets one new row) followed by decode attention of
 every query head -- run as the fused step, two kernels: the partial kernel
-(which also performs the append) and the merge (which also advances len).  The default workload is
+(which also performs the append) and the merge (which also advances len);
+this is da_decode_step, called as its two halves so that events can bracket
+the partial kernel.  The default workload is
 the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
 len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
 
@@ -24,6 +26,7 @@ Prints ONE JSON line:
                this host on a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c5]
+                       [--graph]   (replay the timed steps as one HIP graph)
 """
 from __future__ import annotations
 
@@ -133,6 +136,8 @@ def main() -> int:
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the timed steps in one HIP graph and replay it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for counter scaling)")
     args = ap.parse_args()
@@ -191,19 +196,20 @@ def main() -> int:
         # the merge (which also advances len) -- da_decode_step, with the
         # partial kernel bracketed by events.
         t = i % nsteps_in
+        st = torch.cuda.current_stream()   # the capture stream inside a graph
         if s.steps and t == 0 and i > 0:
-            dl.copy_(lens0)              # a new pass over the 64-step sequence
+            dl.copy_(lens0)              # a new pass over the multi-step sequence
         if ev_a is not None:
-            ev_a.record(stream)
+            ev_a.record(st)
         if s.steps:
             binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk,
-                                   k_new=dkn[t], v_new=dvn[t], stream=stream)
+                                   k_new=dkn[t], v_new=dvn[t], stream=st)
         else:
-            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=stream)
+            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=st)
         if ev_b is not None:
-            ev_b.record(stream)
+            ev_b.record(st)
         binding.decode_merge(out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
-                             chunk, lens=dl if s.steps else None, stream=stream)
+                             chunk, lens=dl if s.steps else None, stream=st)
 
     log(f"warmup {args.warmup} step(s), chunk_rows={chunk}")
     for i in range(args.warmup):
@@ -223,21 +229,42 @@ def main() -> int:
             lens_host = np.minimum(lens_host + 1, s.n_max)
         step_lens.append(lens_host.copy())
 
-    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
-    log(f"timing {args.steps} step(s)")
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    start.record(stream)
-    for i in range(args.steps):
-        step(i, ev_a[i], ev_b[i])
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = start.elapsed_time(end)
-    partial_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
+    if args.graph:
+        # The timed steps as one graph (the graph holds no memset, and the
+        # workspace counters come back to zero after each step), replayed once
+        # from the same initial state; the per-launch time is then the step's.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(args.steps):
+                step(i)
+        dl.copy_(lens0)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        log(f"timing {args.steps} step(s) as one graph replay")
+        wall0 = time.perf_counter()
+        start.record(stream)
+        graph.replay()
+        end.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        total_ms = start.elapsed_time(end)
+        launch_ms = [total_ms / args.steps] * args.steps
+    else:
+        ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        log(f"timing {args.steps} step(s)")
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        start.record(stream)
+        for i in range(args.steps):
+            step(i, ev_a[i], ev_b[i])
+        end.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        total_ms = start.elapsed_time(end)
+        launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
 
     def step_bytes(lens, with_append=True):
         b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v)
@@ -248,12 +275,12 @@ def main() -> int:
     alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
     # The partial kernel of a step also writes the appended rows (Prop. 2).
     append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v) if s.steps else 0
-    partial_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
-                     for l in step_lens]
+    launch_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
+                    for l in step_lens]
     ms_per_step = total_ms / args.steps
     value = alg_bytes / (total_ms * 1e-3) / 1e9
-    part_avg_ms = sum(partial_ms) / len(partial_ms)
-    achieved = (sum(partial_bytes) / len(partial_bytes)) / (part_avg_ms * 1e-3) / 1e9
+    launch_avg_ms = sum(launch_ms) / len(launch_ms)
+    achieved = (sum(launch_bytes) / len(launch_bytes)) / (launch_avg_ms * 1e-3) / 1e9
 
     result = {
         "metric": METRIC,
@@ -275,8 +302,9 @@ def main() -> int:
             "initial_len": [int(x) for x in inp.lens],
             "steps_per_sequence": s.steps,
             "chunk_rows": chunk,
-            "step": "decode_partial with fused kv_append + decode_merge" if s.steps
-                    else "decode_partial + decode_merge",
+            "step": ("decode_partial with fused kv_append + decode_merge" if s.steps
+                     else "decode_partial + decode_merge"),
+            "graph": bool(args.graph),
         },
         "us_per_step": round(ms_per_step * 1e3, 2),
         "hbm_roofline_frac_step": round(value / HBM_PEAK_GBPS, 4),
@@ -290,12 +318,14 @@ def main() -> int:
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": counter_traffic(s.name),
-            "avg_launch_us": round(part_avg_ms * 1e3, 2),
-            "algorithmic_bytes_per_launch": int(sum(partial_bytes) / len(partial_bytes)),
+            "avg_launch_us": round(launch_avg_ms * 1e3, 2),
+            "timing": ("graph replay / steps (partial + merge)" if args.graph
+                       else "HIP events around each partial launch"),
+            "algorithmic_bytes_per_launch": int(sum(launch_bytes) / len(launch_bytes)),
         },
     }
     log(f"{ms_per_step * 1e3:.1f} us/step, {value:.0f} GB/s; partial "
-        f"{part_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
+        f"{launch_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
 
     del dK, dV
     torch.cuda.empty_cache()

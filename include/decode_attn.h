@@ -71,14 +71,15 @@ const char *da_status_string(int status);
 /*
  * Workspace.  The decode keeps, per (b, query head), a few partial results
  * (running maximum, running sum of exponentials, unnormalised weighted sum of
- * V rows) plus three small counters per (b, KV head) that schedule the work.
- * The counter region -- the first da_decode_workspace_counter_bytes() bytes
- * -- must be zero before the first decode that uses the workspace (an
- * all-zero workspace always qualifies); every completed decode (partial then
- * merge) leaves it zero again, so a workspace can be reused call after call
- * without clearing.  The rest of the workspace needs no initialisation.  One
- * workspace serves one decode at a time: decodes that overlap in time (on
- * different streams) need separate workspaces.
+ * V rows) plus a few counters per (b, KV head) that schedule the work.  The
+ * counter region -- the first da_decode_workspace_counter_bytes() bytes --
+ * must be zero before the first decode that uses the workspace (an all-zero
+ * workspace always qualifies); every completed decode leaves it zero again,
+ * so a workspace can be reused call after call without clearing (and a call
+ * can be captured in a HIP graph and replayed).  The rest of the workspace
+ * needs no initialisation.  One workspace serves one decode at a time:
+ * decodes that overlap in time (on different streams) need separate
+ * workspaces.
  */
 
 /*
@@ -88,9 +89,10 @@ const char *da_status_string(int status);
 int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
 
 /*
- * Bytes of device workspace da_decode_attn / da_decode_partial /
- * da_decode_merge need for these shapes and chunk size (0 = the library's
- * choice).  Returns 0 if the shapes or chunk_rows are invalid.
+ * Bytes of device workspace da_decode_attn / da_decode_step /
+ * da_decode_partial + da_decode_merge need for these shapes and chunk size
+ * (0 = the library's choice).  Returns 0 if the shapes or chunk_rows are
+ * invalid.
  */
 size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
                                  int d_v, int chunk_rows);
@@ -116,11 +118,10 @@ size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
  * the library's choice) that a resident set of workgroups takes dynamically;
  * a workgroup folds every chunk it takes from one slab into one running
  * softmax state (the online form of eq. (2)) and leaves one partial per
- * visit;
- * the partials are then combined exactly (a regrouping of eqs. (2)-(3) over
- * disjoint row sets).  The summation order therefore varies from call to call
- * within fp32 rounding.  Equivalent to da_decode_partial followed by
- * da_decode_merge.
+ * visit; a second launch combines the partials exactly (a regrouping of eqs.
+ * (2)-(3) over disjoint row sets).  The summation order therefore varies
+ * from call to call within fp32 rounding.  Equivalent to da_decode_partial
+ * followed by da_decode_merge.
  *
  * Supported: d_k, d_v in {64, 128}; any B, h_q, h_kv >= 1 with h_kv | h_q.
  * workspace: see above; at least da_decode_workspace_bytes(...) bytes,
@@ -136,10 +137,10 @@ da_status da_decode_attn(const float *q, const float *K, const float *V,
  * Append and decode in one step: the effect of da_kv_append(K, V, k_new,
  * v_new, len, ...) followed by da_decode_attn(q, K, V, len, ...) -- eqs.
  * (6)-(7) then (1)-(3), the order of one autoregressive step of the paper's
- * multi-step cache -- in two kernel launches instead of three: the decode
- * reads the new row of each KV head straight from k_new / v_new (and writes
- * it into the cache meanwhile), and the merge advances len.  Same results,
- * same argument rules as the two calls; k_new [B][h_kv][d_k] and
+ * multi-step cache -- in two kernel launches instead of three: the partial
+ * launch reads the new row of each KV head straight from k_new / v_new (and
+ * writes it into the cache meanwhile), and the merge advances len.  Same
+ * results, same argument rules as the two calls; k_new [B][h_kv][d_k] and
  * v_new [B][h_kv][d_v] must not overlap K / V.
  */
 da_status da_decode_step(const float *q, float *K, float *V,
@@ -156,7 +157,7 @@ da_status da_decode_step(const float *q, float *K, float *V,
  * k_new and v_new are both NULL (plain decode; K and V are only read) or both
  * set (the fused append of da_decode_step: row len[b] of every KV head is
  * taken from them and written into K / V).  Must be followed by
- * da_decode_merge on the same workspace, which also re-zeroes the counters.
+ * da_decode_merge on the same workspace, which also resets the counters.
  */
 da_status da_decode_partial(const float *q, float *K, float *V,
                             const float *k_new, const float *v_new,

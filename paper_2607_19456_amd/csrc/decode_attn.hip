@@ -2,19 +2,21 @@
 // attention over a KV cache (MHA/GQA/MQA) and the per-step KV append.
 //
 // Kernels
-//   kv_append_kernel       eqs. (6)-(7): one bit-exact row copy per KV head,
-//                          then len[b] += 1 (Proposition 2's (d_k+d_v)*4 B).
-//   decode_partial_kernel  eqs. (1)-(3) over one split of one KV slab, for all
-//                          query heads of its GQA group at once: the slab's
-//                          rows are read from HBM once and feed every head of
-//                          the group (the group caching of the GQA section).
-//   decode_merge_kernel    combines split partials into the output row.
+//   kv_append_kernel  eqs. (6)-(7): one bit-exact row copy per KV head, then
+//                     len[b] += 1 (Proposition 2's (d_k+d_v)*4 bytes).
+//   decode_partial_kernel  eqs. (1)-(3) for all query heads of each GQA group
+//                          at once, as per-visit partial states: every KV slab
+//                          is read from HBM once and feeds all heads of its
+//                          group (the group caching of the GQA section).
+//                          Optionally fused with the append of the same step.
+//   decode_merge_kernel    combines each head's partials into its output row
+//                          and resets the scheduling state.
 //
 // Work decomposition of decode_partial_kernel
-//   grid  (split p, KV head g x head group, batch b), 256 threads = 4 waves.
-//   A workgroup owns rows [p*S, min((p+1)*S, n_b)) of slab (b, g); its waves
-//   take 16-row tiles round-robin.  Each tile is two dense products on the
-//   matrix cores (v_mfma_f32_16x16x4_f32, fp32 in and out):
+//   A resident grid of 256-thread workgroups (4 waves) takes chunks of slab
+//   rows dynamically; a workgroup's waves take the chunk's 16-row tiles
+//   round-robin.  Each tile is two dense products on the matrix cores
+//   (v_mfma_f32_16x16x4_f32, fp32 in and out):
 //     scores  S[16 rows x 16 heads] = K_tile[16 x d_k] . Q^T[d_k x 16]
 //     update  O^T[d_v x 16 heads]  += V_tile^T[d_v x 16] . P[16 x 16 heads]
 //   with the online (running max / running sum) form of the softmax between
@@ -50,7 +52,6 @@ constexpr int kHeadsPerBlock = 16;                   // heads per MFMA column bl
 constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgroup
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
-constexpr int kResidentWorkgroups = kComputeUnits * 2;  // upper bound of the resident set
 // Register tiles per wave in the load ring, and waves per SIMD, of the
 // partial kernel: a three-tile ring at one wave per SIMD keeps two tiles'
 // loads in flight during each tile's products.  (Measured alternatives: two
@@ -67,11 +68,10 @@ constexpr int kDefaultChunkRows = 768;
 // Visit slots per slab, in units of the even share of waves per slab.
 constexpr int kVisitSlack = 4;
 constexpr int64_t kMaxSlabs = 1 << 20;
-// Each slab's three scheduling counters (chunks taken, visits opened, merge
-// workgroups done) share one 128-byte line of their own: atomics on counters
-// of different slabs then never serialize on the same line.
+// Each slab's scheduling word, {chunks taken (low half), visits opened (high
+// half)}, has a 128-byte line of its own, so atomics on different slabs'
+// words never serialize on the same line.
 constexpr int kCounterStride = 32;
-constexpr int kCtr = 0, kVis = 1, kDone = 2;
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ f4 mfma_16x16x4(float a, float b, f4 c) {
@@ -163,9 +163,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Split partials.
-//   ws_ml  [B][h_q][P] float2 (running max in base-2 units, running sum)
-//   ws_acc [B][h_q][P][DV]    unnormalised weighted sum of V rows
+// Register tiles and tile processing of the decode.
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB>
 struct Tile {
@@ -175,17 +173,39 @@ struct Tile {
 
 // Where a tile's rows live: the slab, except row `new_row` (the row a fused
 // append adds; -1 if none), which is read from the incoming k_new / v_new rows.
+// Rows [0, fast_end) are plain slab rows.
 struct RowSource {
   const float* __restrict__ Ks;
   const float* __restrict__ Vs;
   const float* __restrict__ k_new_row;
   const float* __restrict__ v_new_row;
   int new_row;
+  int fast_end;
+  uint32_t k_lane;          // byte offset of lane (i,k) in a K tile: i*d_k + 4k floats
+  uint32_t v_lane;          // byte offset of lane (i,k) in a V tile: 4k*d_v + 4i floats
 };
 
 template <int DK, int DV, int NB>
 __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& src,
                                           int row0, int last_row, int i, int k) {
+  if (row0 + kTileRows <= src.fast_end) {
+    // Interior tile: one wave-uniform row base and a fixed per-lane offset,
+    // so every load is scalar base + lane offset + immediate (no per-tile
+    // address arithmetic on the vector ALUs).
+    const char* kb = reinterpret_cast<const char*>(src.Ks + (int64_t)row0 * DK);
+    const char* vb = reinterpret_cast<const char*>(src.Vs + (int64_t)row0 * DV);
+#pragma unroll
+    for (int t = 0; t < DK / 16; ++t)
+      T.k[t] = load4_stream(reinterpret_cast<const float*>(kb + src.k_lane) + 16 * t);
+#pragma unroll
+    for (int rho = 0; rho < 4; ++rho)
+#pragma unroll
+      for (int c = 0; c < DV / 64; ++c)
+        T.v[rho][c] = load4_stream(reinterpret_cast<const float*>(vb + src.v_lane) + rho * DV + 64 * c);
+    return;
+  }
+  // The slab's last tile: rows past the end clamp to the last row, and the
+  // row a fused append adds comes from k_new / v_new.
   const int rk = min(row0 + i, last_row);
   const float* kp = rk == src.new_row ? src.k_new_row : src.Ks + (int64_t)rk * DK;
 #pragma unroll
@@ -275,7 +295,7 @@ __device__ __forceinline__ int slab_rows(const int32_t* __restrict__ len, int s,
   return decode_rows(len[s / per_b], n_max, app);
 }
 
-__device__ __forceinline__ unsigned load_counter(const unsigned* p) {
+__device__ __forceinline__ unsigned long long load_word(const unsigned long long* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -294,8 +314,9 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
     bool open = false;
     if (o < budget) {
       const int nch = (slab_rows(len, sl, per_b, n_max, app) + C - 1) / C;
-      const unsigned* c = cnt + (size_t)sl * kCounterStride;
-      open = (int)load_counter(c + kCtr) < nch && (int)load_counter(c + kVis) < J;
+      const unsigned long long w = load_word(
+          reinterpret_cast<const unsigned long long*>(cnt + (size_t)sl * kCounterStride));
+      open = (unsigned)w < (unsigned)nch && (unsigned)(w >> 32) < (unsigned)J;
     }
     const unsigned long long m = __ballot(open);
     if (m) {
@@ -314,29 +335,33 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //
 // A slab is the cache rows of one (b, KV head, head group); it is cut into
 // chunks of C rows handed out by a per-slab counter.  A fixed set of
-// workgroups (two per CU for groups of <= 16 heads) stays resident; each one
-// opens a "visit" on a slab with chunks left (slot j = vis++, at most J per
-// slab), takes chunks from that slab's counter until none are left -- its four
-// waves interleave the chunk's 16-row tiles, so the workgroup streams one
-// contiguous run of K and of V -- and folds all of them into one running
-// (max, sum, weighted sum) state, since the online softmax does not care which
-// rows it has seen.  It then writes one partial for the visit to slot j and
-// looks for the next slab.  No CU idles while rows remain and faster CUs
-// simply take more chunks.
+// workgroups (one per CU) stays resident; each one opens a "visit" on a slab
+// with chunks left (taking, in one atomic step, its first two chunks and a
+// visit slot j < J, so every visit has rows and the slots in use are exactly
+// 0 .. visits-1), takes chunks from that slab's counter until none are left
+// -- its four waves interleave the chunk's 16-row tiles, so the workgroup
+// streams one contiguous run of K and of V -- and folds all of them into one
+// running (max, sum, weighted sum) state, since the online softmax does not
+// care which rows it has seen.  It then writes one partial per query head to
+// slot j, counts the visit in each head's visit count and looks for the next
+// slab.  No CU idles while rows remain and faster CUs simply take more chunks.
+// Nothing here waits on another workgroup or needs a device-wide fence: the
+// merge, a separate launch, sees every partial.
 //
-//   counters   per slab {ctr, vis, done}, one 128-byte line each; zero on
-//              entry, reset by the merge
-//   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum);
-//                                        max = -inf marks a visit that got no rows
+//   slab line  per slab one 128-byte line: a 64-bit word {chunks taken (low),
+//              visits opened (high)}; reset by the merge
+//   nvis       [B][h_q] uint32 visits per query head; reset by the merge
+//   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum)
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB>
 __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_kernel(
     const float* __restrict__ q, float* __restrict__ K,
     float* __restrict__ V, const float* __restrict__ k_new,
-    const float* __restrict__ v_new, const int32_t* __restrict__ len,
-    float qscale, int B, int h_q, int h_kv, int n_max, int C, int head_groups, int J,
-    unsigned* __restrict__ cnt, float2* __restrict__ ws_ml, float* __restrict__ ws_acc) {
+    const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
+    int B, int h_q, int h_kv, int n_max, int C, int head_groups, int J,
+    unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
+    float* __restrict__ ws_acc) {
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
@@ -345,7 +370,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // wave-uniform
   const int i = lane & 15;
   const int k = lane >> 4;
 
@@ -377,12 +402,13 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       }
     }
   }
-
   int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
 
   while (true) {
-    // ---- wave 0 opens a visit: a slab with chunks and slots left, its visit
-    // slot and its first two chunks (lane 0 does the atomics).
+    // ---- wave 0 opens a visit: a slab with chunks and slots left.  Lane 0
+    // takes the slot and the first two chunks with one compare-and-swap on
+    // the slab's {chunks, visits} word, so every visit has at least one
+    // chunk and there are never more than J of them.
     if (wave == 0) {
       int s = -1, j = -1, c = -1, cn = -1;
       int budget = S;
@@ -394,32 +420,27 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
         budget -= seen;
         start = cand + 1 == S ? 0 : cand + 1;
         const int nch = (slab_rows(len, cand, per_b, n_max, app) + C - 1) / C;
-        int slot = -1, got = -1, nxt = -1;
+        unsigned long long got = ~0ull;
         if (lane == 0) {
-          unsigned* cc = cnt + (size_t)cand * kCounterStride;
-          slot = (int)atomicAdd(cc + kVis, 1u);
-          if (slot < J) {
-            got = (int)atomicAdd(cc + kCtr, 1u);
-            nxt = got < nch ? (int)atomicAdd(cc + kCtr, 1u) : nch;
+          unsigned long long* w =
+              reinterpret_cast<unsigned long long*>(cnt + (size_t)cand * kCounterStride);
+          unsigned long long old = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          // Lock-free: a failed swap means another workgroup moved the word.
+          while ((unsigned)old < (unsigned)nch && (unsigned)(old >> 32) < (unsigned)J) {
+            const unsigned long long seen_w = atomicCAS(w, old, old + (1ull << 32) + 2ull);
+            if (seen_w == old) {
+              got = old;
+              break;
+            }
+            old = seen_w;
           }
         }
-        slot = __shfl(slot, 0);
-        if (slot >= J) continue;                        // slab full of visitors
         got = __shfl(got, 0);
-        if (got >= nch) {
-          // The slot is ours but the chunks ran out meanwhile: mark it empty.
-          const int b = cand / per_b;
-          const int rem = cand - b * per_b;
-          const int g = rem / head_groups;
-          const int hgrp = rem - g * head_groups;
-          const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
-          if (lane < h_count) {
-            const int h = g * G + hgrp * (NB * kHeadsPerBlock) + lane;
-            ws_ml[((int64_t)b * h_q + h) * J + slot] = make_float2(-INFINITY, 0.f);
-          }
-          continue;
-        }
-        s = cand; j = slot; c = got; cn = __shfl(nxt, 0);
+        if (got == ~0ull) continue;                     // no chunk or slot left meanwhile
+        s = cand;
+        j = (int)(got >> 32);
+        c = (int)(unsigned)got;
+        cn = c + 1;
         break;
       }
       if (lane == 0) { sh_ctl[0] = s; sh_ctl[1] = j; sh_ctl[2] = c; sh_ctl[3] = cn; }
@@ -442,12 +463,17 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
     const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
     const int64_t slab = (int64_t)b * h_kv + g;
+    unsigned long long* slab_word =
+        reinterpret_cast<unsigned long long*>(cnt + (size_t)s * kCounterStride);
     RowSource src;
     src.Ks = K + slab * n_max * DK;
     src.Vs = V + slab * n_max * DV;
     src.new_row = appends(app, len_b, n_max) ? len_b : -1;
+    src.fast_end = src.new_row >= 0 ? src.new_row : n;
     src.k_new_row = app ? k_new + slab * DK : nullptr;
     src.v_new_row = app ? v_new + slab * DV : nullptr;
+    src.k_lane = (uint32_t)(i * DK + 4 * k) * sizeof(float);
+    src.v_lane = (uint32_t)(4 * k * DV + 4 * i) * sizeof(float);
 
     // B operand of the score product, staged in LDS in register order: entry
     // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
@@ -497,7 +523,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       // counter simply runs past the end): a conditional request would merge
       // its result with another value right here and force a wait for it.
       int after;
-      if (tid == 0) after = (int)atomicAdd(cnt + (size_t)s * kCounterStride + kCtr, 1u);
+      if (tid == 0) after = (int)(unsigned)atomicAdd(slab_word, 1ull);
       // A loop that always runs at least once and exits at its bottom: after
       // its first wait on a tile load the compiler knows the atomic issued
       // above (an older memory operation) has returned, so publishing its
@@ -544,7 +570,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     }
 
     // Combine the 4 waves: waves 1..3 park their state in LDS in their own
-    // register layout; wave 0 rescales and adds it lane by lane.
+    // register layout; wave 0 rescales and adds it lane by lane, writes the
+    // visit's partial and counts the visit for each of its heads.
     if (wave > 0) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
@@ -582,8 +609,12 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
         }
         const int hl = nb * kHeadsPerBlock + i;
         if (hl < h_count) {
-          const int64_t slot = ((int64_t)b * h_q + h_first + hl) * J + j;
-          if (k == 0) ws_ml[slot] = make_float2(M, L);
+          const int64_t head = (int64_t)b * h_q + h_first + hl;
+          const int64_t slot = head * J + j;
+          if (k == 0) {
+            ws_ml[slot] = make_float2(M, L);
+            atomicAdd(nvis + head, 1u);
+          }
           float* dst = ws_acc + slot * DV;
 #pragma unroll
           for (int cc = 0; cc < DV / 64; ++cc)
@@ -602,21 +633,24 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
 }
 
 // ---------------------------------------------------------------------------
-// Merge, one workgroup per (slab, query head of its group):
-//   out[b,h,:] = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j
-// over the slab's min(vis[s], J) visit partials (empty visits, m = -inf, are
-// skipped).  Threads split the visits 8 ways and the 16-byte columns 32 ways
-// (d_v = 128), then combine through LDS.  The last workgroup of a slab to
-// finish resets the slab's three counters to zero for the next call.
+// Merge, one workgroup per (slab, query head of its group): eqs. (2)-(3)
+// regrouped over disjoint row sets,
+//   out[b,h,:] = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j,  M = max_j m_j,
+// over the head's nv visit partials (nv = 0: an empty cache, out = 0).
+// Threads split the visits kLanesV ways and the 16-byte columns DV/4 ways,
+// then combine through LDS.  Every piece of scheduling state is reset by the
+// one workgroup that owns it -- the head's visit count by its workgroup, the
+// slab's line by the slab's first head -- so the next call finds zeros, with
+// no atomics and no device-wide fences.
 // ---------------------------------------------------------------------------
 template <int DV>
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
     float* __restrict__ out, const float2* __restrict__ ws_ml,
     const float* __restrict__ ws_acc, int h_q, int h_kv, int head_groups, int heads_per_group,
-    int merge_heads, int J, unsigned* __restrict__ cnt, int32_t* __restrict__ len_bump,
-    int n_max) {
-  constexpr int kChunks = DV / 4;                       // 16-byte columns per row
-  constexpr int kLanesV = kThreads / kChunks;           // visits merged in parallel
+    int merge_heads, int J, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis,
+    int32_t* __restrict__ len_bump, int n_max) {
+  constexpr int kCols = DV / 4;                         // 16-byte columns per row
+  constexpr int kLanesV = kThreads / kCols;             // visits merged in parallel
   const int s = blockIdx.x / merge_heads;
   const int hl = blockIdx.x - s * merge_heads;
   const int per_b = h_kv * head_groups;
@@ -627,61 +661,62 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
   const int G = h_q / h_kv;
   const int h_count = min(heads_per_group, G - hgrp * heads_per_group);
   if (hl >= h_count) return;                            // padding workgroup
-  // Completing a fused append: len[b] advances once per sequence, after the
-  // partial kernel (which read it) has finished.
-  if (len_bump && g == 0 && hgrp == 0 && hl == 0 && threadIdx.x == 0) {
-    const int32_t t = len_bump[b];
-    if (t >= 0 && t < n_max) len_bump[b] = t + 1;
-  }
-  unsigned* slab_cnt = cnt + (size_t)s * kCounterStride;
-  const int nv = min((int)slab_cnt[kVis], J);
-  const int ch = threadIdx.x % kChunks;
-  const int pv = threadIdx.x / kChunks;
+  const int tid = threadIdx.x;
   const int64_t row = (int64_t)b * h_q + g * G + hgrp * heads_per_group + hl;
+  const int nv = min((int)nvis[row], J);
+  const int ch = tid % kCols;
+  const int pv = tid / kCols;
   const float2* ml = ws_ml + row * J;
   const float* acc = ws_acc + row * J * DV;
 
-  float m = -INFINITY, l = 0.f;
+  // This lane's visits pv, pv + kLanesV, ...: their maximum, then the
+  // rescaled sums (all loads of a pass are independent).
+  float m = -INFINITY;
+#pragma unroll 4
+  for (int jj = pv; jj < nv; jj += kLanesV) m = fmaxf(m, ml[jj].x);
+  float l = 0.f;
   f4 o = f4{0.f, 0.f, 0.f, 0.f};
-  for (int jj = pv; jj < nv; jj += kLanesV) {
-    const float2 st = ml[jj];
-    if (st.x == -INFINITY) continue;                    // an empty visit
-    const float mn = fmaxf(m, st.x);
-    const float a = fast_exp2(m - mn);                  // m = -inf: 0
-    const float w = fast_exp2(st.x - mn);
-    l = l * a + st.y * w;
-    o = o * a + load4(acc + (int64_t)jj * DV + 4 * ch) * w;
-    m = mn;
+  if (m != -INFINITY) {
+#pragma unroll 4
+    for (int jj = pv; jj < nv; jj += kLanesV) {
+      const float2 st = ml[jj];
+      const float w = fast_exp2(st.x - m);
+      l += st.y * w;
+      o += load4(acc + (int64_t)jj * DV + 4 * ch) * w;
+    }
   }
   __shared__ float sh_m[kThreads], sh_l[kThreads];
   __shared__ f4 sh_o[kThreads];
-  sh_m[threadIdx.x] = m;
-  sh_l[threadIdx.x] = l;
-  sh_o[threadIdx.x] = o;
+  sh_m[tid] = m;
+  sh_l[tid] = l;
+  sh_o[tid] = o;
   __syncthreads();
   if (pv == 0) {
     float M = m;
-    for (int p = 1; p < kLanesV; ++p) M = fmaxf(M, sh_m[p * kChunks + ch]);
+    for (int p = 1; p < kLanesV; ++p) M = fmaxf(M, sh_m[p * kCols + ch]);
     float L = 0.f;
     f4 O = f4{0.f, 0.f, 0.f, 0.f};
     if (M != -INFINITY) {
       for (int p = 0; p < kLanesV; ++p) {
-        const float w = fast_exp2(sh_m[p * kChunks + ch] - M);
-        L += sh_l[p * kChunks + ch] * w;
-        O += sh_o[p * kChunks + ch] * w;
+        const float w = fast_exp2(sh_m[p * kCols + ch] - M);
+        L += sh_l[p * kCols + ch] * w;
+        O += sh_o[p * kCols + ch] * w;
       }
     }
-    // No visit (empty cache): the output row is zero.
     *reinterpret_cast<f4*>(out + row * DV + 4 * ch) = M != -INFINITY ? O / L : f4{0.f, 0.f, 0.f, 0.f};
   }
-  if (threadIdx.x == 0) {
-    // Every workgroup of the slab read vis[s] above (nv is already in use);
-    // the last one to get here clears the slab's counters.
-    __threadfence();
-    if (atomicAdd(slab_cnt + kDone, 1u) == (unsigned)h_count - 1u) {
-      slab_cnt[kVis] = 0u;
-      slab_cnt[kCtr] = 0u;
-      slab_cnt[kDone] = 0u;
+  if (tid == 0) {
+    nvis[row] = 0u;
+    if (hl == 0) {
+      // The slab's line: read by no merge workgroup, so its first head's
+      // workgroup clears it.
+      *reinterpret_cast<unsigned long long*>(cnt + (size_t)s * kCounterStride) = 0ull;
+      // Completing a fused append: len[b] advances once per sequence, after
+      // the partial kernel (which read it) has finished.
+      if (len_bump && g == 0 && hgrp == 0) {
+        const int32_t t = len_bump[b];
+        if (t >= 0 && t < n_max) len_bump[b] = t + 1;
+      }
     }
   }
 }
@@ -690,14 +725,14 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
 // Host side: validation, sizing, launches.
 // ---------------------------------------------------------------------------
 struct Plan {
-  int chunk_rows;     // rows per dynamically scheduled chunk (one wave's unit)
+  int chunk_rows;     // rows per dynamically scheduled chunk
   int head_groups;    // groups of up to 32 query heads per KV head
   int blocks;         // MFMA column blocks per wave (1 or 2)
   int slabs;          // B * h_kv * head_groups
   int grid;           // resident workgroups of the partial kernel
   int J;              // visit slots per (b, query head)
   int merge_heads;    // query heads per slab the merge covers
-  size_t counter_bytes, ml_bytes, bytes;
+  size_t line_bytes, counter_bytes, ml_bytes, bytes;
 };
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -732,20 +767,23 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int64_t resident = (int64_t)kComputeUnits * (plan->blocks == 1 ? kWavesPerSimd<1>
                                                                         : kWavesPerSimd<2>);
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
-  // A slab is visited at most once per workgroup and per chunk; kVisitSlack
-  // times the even share of workgroups per slab leaves room for workgroups
-  // that move on from finished slabs.
+  // Every visit holds at least one chunk; kVisitSlack times the even share
+  // of workgroups per slab leaves room for workgroups that move on from
+  // finished slabs.
   const int64_t share = ceil_div((int64_t)plan->grid, plan->slabs);
   plan->J = (int)std::max<int64_t>(1, std::min(chunks_per_slab, kVisitSlack * share));
-  const size_t slots = (size_t)B * h_q * plan->J;
-  plan->counter_bytes = pad256((size_t)plan->slabs * kCounterStride * sizeof(unsigned));
+  const size_t heads = (size_t)B * h_q;
+  const size_t slots = heads * plan->J;
+  plan->line_bytes = pad256((size_t)plan->slabs * kCounterStride * sizeof(unsigned));
+  plan->counter_bytes = plan->line_bytes + pad256(heads * sizeof(unsigned));
   plan->ml_bytes = pad256(slots * sizeof(float2));
   plan->bytes = plan->counter_bytes + plan->ml_bytes + slots * (size_t)d_v * sizeof(float);
   return DA_OK;
 }
 
 struct WsView {
-  unsigned* cnt;
+  unsigned* cnt;      // per-slab lines
+  unsigned* nvis;     // per-head visit counts
   float2* ml;
   float* acc;
 };
@@ -754,6 +792,7 @@ WsView view(const Plan& pl, void* workspace) {
   char* base = static_cast<char*>(workspace);
   WsView w;
   w.cnt = reinterpret_cast<unsigned*>(base);
+  w.nvis = reinterpret_cast<unsigned*>(base + pl.line_bytes);
   w.ml = reinterpret_cast<float2*>(base + pl.counter_bytes);
   w.acc = reinterpret_cast<float*>(base + pl.counter_bytes + pl.ml_bytes);
   return w;
@@ -778,7 +817,8 @@ template <int DK, int DV, int NB>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
   hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB>), dim3(pl.grid), dim3(kThreads), 0,
                      stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
-                     a.h_kv, a.n_max, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.ml, w.acc);
+                     a.h_kv, a.n_max, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.nvis, w.ml,
+                     w.acc);
 }
 
 template <int DK, int DV>
@@ -789,17 +829,20 @@ void launch_partial_nb(const Plan& pl, const PartialArgs& a, const WsView& w, hi
     launch_partial<DK, DV, 2>(pl, a, w, s);
 }
 
+// Validation of everything but `out` in the documented order (NULL, shapes,
+// alignment, scale, workspace), then the partial launch.
 da_status partial_impl(const float* q, const float* K, const float* V, const float* k_new,
                        const float* v_new, const int32_t* len, float scale, int B, int h_q,
                        int h_kv, int n_max, int d_k, int d_v, int chunk_rows, void* workspace,
-                       size_t workspace_bytes, void* stream, Plan* out_plan) {
-  if (!q || !K || !V || !len) return DA_ERR_NULL;
+                       size_t workspace_bytes, void* stream, const float* out, bool need_out,
+                       Plan* out_plan) {
+  if (!q || !K || !V || !len || (need_out && !out)) return DA_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return DA_ERR_NULL;
   Plan pl;
   da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4) ||
-      !aligned(k_new, 16) || !aligned(v_new, 16))
+      !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(out, 16))
     return DA_ERR_ALIGN;
   if (!std::isfinite(scale)) return DA_ERR_SCALE;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
@@ -838,11 +881,11 @@ da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, in
   if (d_v == 64)
     hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
                        h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
-                       len_bump, n_max);
+                       w.nvis, len_bump, n_max);
   else
     hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
                        h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
-                       len_bump, n_max);
+                       w.nvis, len_bump, n_max);
   return launch_status();
 }
 
@@ -889,7 +932,7 @@ da_status da_decode_partial(const float* q, float* K, float* V, const float* k_n
                             int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
                             void* workspace, size_t workspace_bytes, void* stream) {
   return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
-                      chunk_rows, workspace, workspace_bytes, stream, nullptr);
+                      chunk_rows, workspace, workspace_bytes, stream, nullptr, false, nullptr);
 }
 
 da_status da_decode_merge(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
@@ -903,17 +946,10 @@ da_status da_decode_attn(const float* q, const float* K, const float* V, const i
                          float scale, float* out, int B, int h_q, int h_kv, int n_max,
                          int d_k, int d_v, int chunk_rows, void* workspace,
                          size_t workspace_bytes, void* stream) {
-  if (!out) return DA_ERR_NULL;
-  if (!aligned(out, 16)) {
-    // Same order as the partial's checks: NULL and shape errors before ALIGN.
-    if (!q || !K || !V || !len) return DA_ERR_NULL;
-    Plan pl;
-    da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
-    return st != DA_OK ? st : DA_ERR_ALIGN;
-  }
   Plan pl;
   da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
-                              d_v, chunk_rows, workspace, workspace_bytes, stream, &pl);
+                              d_v, chunk_rows, workspace, workspace_bytes, stream, out, true,
+                              &pl);
   if (st != DA_OK) return st;
   return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
@@ -923,16 +959,10 @@ da_status da_decode_step(const float* q, float* K, float* V, const float* k_new,
                          const float* v_new, int32_t* len, float scale, float* out, int B,
                          int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
                          void* workspace, size_t workspace_bytes, void* stream) {
-  if (!out || !k_new || !v_new) return DA_ERR_NULL;
-  if (!aligned(out, 16)) {
-    if (!q || !K || !V || !len) return DA_ERR_NULL;
-    Plan pl;
-    da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
-    return st != DA_OK ? st : DA_ERR_ALIGN;
-  }
+  if (!k_new || !v_new) return DA_ERR_NULL;
   Plan pl;
   da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
-                              chunk_rows, workspace, workspace_bytes, stream, &pl);
+                              chunk_rows, workspace, workspace_bytes, stream, out, true, &pl);
   if (st != DA_OK) return st;
   return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
                     workspace_bytes, stream);

@@ -43,8 +43,9 @@ def test_status_strings():
 
 
 def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
-    """The sizing rule the header documents, restated: one visit slot per
-    (b, query head) for up to 4x the even share of resident waves per slab."""
+    """The sizing rule, restated: one visit slot per (b, query head) for up to
+    4x the even share of resident workgroups per slab; one 128-byte counter
+    line per slab and one visit count per (b, query head)."""
     pad = lambda x: -(-x // 256) * 256
     G = h_q // h_kv
     groups = -(-G // 32)
@@ -54,7 +55,7 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     grid = max(1, min(resident, chunks * slabs))
     J = max(1, min(chunks, 4 * -(-grid // slabs)))
     slots = B * h_q * J
-    counters = pad(slabs * 128)
+    counters = pad(slabs * 128) + pad(B * h_q * 4)
     return counters, counters + pad(slots * 8) + slots * d_v * 4
 
 
@@ -100,7 +101,7 @@ def test_decode_validation(kw, status):
     assert _decode(**kw) == status
 
 
-def test_partial_merge_and_step_validation():
+def test_partial_and_merge_validation():
     P = lib.da_decode_partial
     assert P(None, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
              FAKE, 1 << 20, None) == 1
@@ -117,18 +118,26 @@ def test_partial_merge_and_step_validation():
     assert M(FAKE, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None) == 6
     assert M(FAKE + 4, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
     assert M(FAKE, FAKE + 2, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
+
+
+def test_step_validation():
     S = lib.da_decode_step
     args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 1, 1, 64, 64, 64, 0,
             FAKE, 1 << 20, None]
     for pos in (0, 1, 2, 3, 4, 5, 7):
         a = list(args); a[pos] = None
         assert S(*a) == 1, pos
-    a = list(args); a[7] = FAKE + 4
-    assert S(*a) == 4
+    for pos in (3, 4, 7):
+        a = list(args); a[pos] = FAKE + 4
+        assert S(*a) == 4, pos
     a = list(args); a[16] = 8
     assert S(*a) == 6
     a = list(args); a[6] = float("nan")
     assert S(*a) == 5
+    a = list(args); a[9] = 3; a[10] = 2
+    assert S(*a) == 2
+    a = list(args); a[12] = 96
+    assert S(*a) == 3
 
 
 @pytest.mark.parametrize("args,status", [

@@ -156,6 +156,34 @@ def test_large_logits_stay_finite(cuda_device):
     check(got, ref, "large logits")
 
 
+def test_plain_decode_leaves_cache_and_len_alone(cuda_device):
+    shape = workloads.custom("plain", B=2, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=900)
+    inp = workloads.make(shape, seed=9, lens=np.array([900, 450], np.int32))
+    dq, dK, dV, dl = (dev(a, cuda_device) for a in (inp.q, inp.K, inp.V, inp.lens))
+    ws = poisoned_workspace(dq, dK, dV)
+    out = binding.decode_attn(dq, dK, dV, dl, float(shape.scale32()), workspace=ws)
+    torch.cuda.synchronize()
+    assert dl.cpu().numpy().tolist() == [900, 450]
+    assert np.array_equal(dK.cpu().numpy().view(np.uint32), inp.K.view(np.uint32))
+    assert np.array_equal(dV.cpu().numpy().view(np.uint32), inp.V.view(np.uint32))
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(out.cpu().numpy().astype(np.float64), ref, "plain decode")
+
+
+@pytest.mark.parametrize("h_q,h_kv", [(4, 1), (1, 1), (32, 1)])
+def test_one_slab_many_visits(cuda_device, h_q, h_kv):
+    """A single long slab in small chunks: every resident workgroup visits it,
+    so its merge combines hundreds of partials."""
+    n = 150_000
+    shape = workloads.custom(f"one_slab_{h_q}", B=1, h_q=h_q, h_kv=h_kv, d_k=128, d_v=128,
+                             n_max=n)
+    inp = workloads.make(shape, seed=12, lens=np.array([n - 5], np.int32))
+    say(f"one slab h_q={h_q}: decode")
+    got = run_decode(inp, cuda_device, chunk_rows=384)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, f"one slab h_q={h_q}")
+
+
 def test_decode_partial_then_merge_equals_decode(cuda_device):
     shape = workloads.custom("pm", B=2, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=900)
     inp = workloads.make(shape, seed=9, lens=np.array([900, 450], np.int32))
@@ -236,6 +264,57 @@ def test_fused_step_long_context_sampled(cuda_device):
         ref = oracle.decode(inp.q_step[t], hK, hV, hl, shape.scale32(), heads=heads)
         check(out.cpu().numpy().astype(np.float64)[heads], ref[heads], f"fused step {t}")
         assert dl.cpu().numpy().tolist() == hl.tolist()
+
+
+def test_graph_replay_of_fused_steps(cuda_device):
+    """Several fused steps captured in one HIP graph and replayed three times,
+    each replay from the same initial cache with eager work in between: every
+    replay matches the oracle step by step (the kernel holds no memset and
+    leaves the workspace counters zero, so replays are independent)."""
+    T = 4
+    shape = workloads.custom("graph", B=3, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=1200,
+                             steps=T)
+    inp = workloads.make(shape, seed=21, lens=np.array([0, 600, 1198], np.int32))
+    dK0, dV0, dl0 = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    dK, dV, dl = dK0.clone(), dV0.clone(), dl0.clone()
+    qs = [dev(inp.q_step[t], cuda_device) for t in range(T)]
+    kn = [dev(inp.k_new[t], cuda_device) for t in range(T)]
+    vn = [dev(inp.v_new[t], cuda_device) for t in range(T)]
+    ws = binding.alloc_workspace(qs[0], dK, dV)
+    outs = [torch.empty((3, 16, 128), device=cuda_device) for _ in range(T)]
+    scale = float(shape.scale32())
+    # host mirror and oracle outputs of the T steps
+    hK, hV, hl = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    refs = []
+    for t in range(T):
+        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+        refs.append(oracle.decode(inp.q_step[t], hK, hV, hl, shape.scale32()))
+    # one eager pass first (loads the kernels before capture)
+    for t in range(T):
+        binding.decode_step(qs[t], dK, dV, kn[t], vn[t], dl, scale, out=outs[t], workspace=ws)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for t in range(T):
+            binding.decode_step(qs[t], dK, dV, kn[t], vn[t], dl, scale, out=outs[t],
+                                workspace=ws)
+    for rep in range(3):
+        dK.copy_(dK0)
+        dV.copy_(dV0)
+        dl.copy_(dl0)
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        say(f"graph replay {rep}")
+        graph.replay()
+        torch.cuda.synchronize()
+        for t in range(T):
+            check(outs[t].cpu().numpy().astype(np.float64), refs[t], f"replay {rep} step {t}")
+        assert dl.cpu().numpy().tolist() == hl.tolist()
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))
+        assert np.array_equal(dV.cpu().numpy().view(np.uint32), hV.view(np.uint32))
+        nc = binding.workspace_counter_bytes(3, 16, 2, 1200, 128, 128)
+        assert not ws[:nc].any()
 
 
 # --- append: bit-exact --------------------------------------------------------
