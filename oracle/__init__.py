@@ -14,6 +14,10 @@ Functions follow the paper as follows:
 * :func:`decode_weights` -- Step II's weight vector for one (b, h).
 * :func:`append` -- the concatenation append of eqs. (6)-(7) with the
   pre-allocated cache semantics of the "moa_kvcache" listing.
+* :func:`decode_multi` -- T query rows per head with causal visibility (the
+  rank-2 query of the paper's training form, for a step that submits several
+  positions at once): each row is Algorithm 1 on its causal prefix.
+* :func:`append_rows` -- :func:`append` applied T times in order.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against the paper's
 worked examples, closed forms, invariants, a high-precision brute force and
@@ -72,6 +76,12 @@ def _configure(lib):
     lib.oracle_append.argtypes = [f32p, f32p, f32p, f32p, i32p,
                                   ci, ci, ci, ci, ci]
     lib.oracle_append.restype = ci
+    lib.oracle_decode_multi.argtypes = [f32p, f32p, f32p, i32p, ctypes.c_float,
+                                        f64p, ci, ci, ci, ci, ci, ci, ci, ci]
+    lib.oracle_decode_multi.restype = ci
+    lib.oracle_append_rows.argtypes = [f32p, f32p, f32p, f32p, i32p,
+                                       ci, ci, ci, ci, ci, ci]
+    lib.oracle_append_rows.restype = ci
     lib.oracle_max_threads.argtypes = []
     lib.oracle_max_threads.restype = ci
     _lib = lib
@@ -197,3 +207,51 @@ def append(K, V, k_new, v_new, lens) -> None:
                            _ptr(lens, ctypes.c_int32), B, h_kv, n_max, d_k, d_v)
     if rc != 0:
         raise ValueError("oracle_append rejected the shapes")
+
+
+def decode_multi(q, K, V, lens, scale, threads: int = 0) -> np.ndarray:
+    """Decode with T query rows per (b, h): returns ``out[B, h_q, T, d_v]``
+    (fp64).  q[B,h_q,T,d_k]; row r of sequence b sits at cache position
+    clamp(len[b]) - T + r and attends rows 0..that position."""
+    lib = _load()
+    q = _f32(q, "q", 4)
+    K = _f32(K, "K", 4)
+    V = _f32(V, "V", 4)
+    B, h_q, T, d_k = q.shape
+    Bk, h_kv, n_max, d_k2 = K.shape
+    Bv, h_kv2, n_max2, d_v = V.shape
+    if not (Bk == Bv == B and h_kv2 == h_kv and n_max2 == n_max and d_k2 == d_k):
+        raise ValueError("inconsistent q/K/V shapes")
+    lens = _lens(lens, B)
+    out = np.full((B, h_q, T, d_v), np.nan, dtype=np.float64)
+    rc = lib.oracle_decode_multi(_ptr(q, ctypes.c_float), _ptr(K, ctypes.c_float),
+                                 _ptr(V, ctypes.c_float), _ptr(lens, ctypes.c_int32),
+                                 ctypes.c_float(np.float32(scale)),
+                                 _ptr(out, ctypes.c_double), B, h_q, h_kv, n_max,
+                                 d_k, d_v, T, int(threads))
+    if rc != 0:
+        raise ValueError("oracle_decode_multi rejected the shapes")
+    return out
+
+
+def append_rows(K, V, k_new, v_new, lens) -> None:
+    """T rows appended in order (k_new[B,h_kv,T,d_k], v_new[B,h_kv,T,d_v]);
+    ``lens`` is updated in place."""
+    lib = _load()
+    K = _f32(K, "K", 4)
+    V = _f32(V, "V", 4)
+    B, h_kv, n_max, d_k = K.shape
+    d_v = V.shape[3]
+    k_new = _f32(k_new, "k_new", 4)
+    v_new = _f32(v_new, "v_new", 4)
+    T = k_new.shape[2]
+    if k_new.shape != (B, h_kv, T, d_k) or v_new.shape != (B, h_kv, T, d_v):
+        raise ValueError("k_new/v_new shapes do not match the cache")
+    if not (isinstance(lens, np.ndarray) and lens.dtype == np.int32
+            and lens.shape == (B,) and lens.flags.c_contiguous):
+        raise TypeError("lens must be a contiguous int32 array of shape (B,)")
+    rc = lib.oracle_append_rows(_ptr(K, ctypes.c_float), _ptr(V, ctypes.c_float),
+                                _ptr(k_new, ctypes.c_float), _ptr(v_new, ctypes.c_float),
+                                _ptr(lens, ctypes.c_int32), B, h_kv, n_max, d_k, d_v, T)
+    if rc != 0:
+        raise ValueError("oracle_append_rows rejected the shapes")

@@ -23,6 +23,9 @@
  *   len [B]            number of valid cache rows of sequence b
  *   out [B][h_q][d_v]  (fp64)
  *
+ * Multi-row decode (oracle_decode_multi): q [B][h_q][T][d_k] and
+ * out [B][h_q][T][d_v]; the T query rows are the cache's last T positions.
+ *
  * Readings of points the paper leaves open (each also stated beside the code
  * that implements it):
  *   - scale multiplies the dot product once, eq. (1); it is always passed in.
@@ -207,6 +210,99 @@ int oracle_append(float *K, float *V, const float *k_new, const float *v_new,
                    sizeof(float) * (size_t)d_v);
         }
         len[b] = t + 1;
+    }
+    return 0;
+}
+
+/*
+ * Decode with T query rows per (b, h): the rank-2 query of the paper's
+ * training form, softmax(scale * Q (+.x Omega<2,2>) K) (+.x Omega<2,2>) V,
+ * restricted to causal visibility for a step that submits T consecutive
+ * positions at once (speculative verification, chunked prefill).  The T rows
+ * occupy the cache's last T positions: row r of sequence b sits at position
+ *   p = clamp(len[b], 0, n_max) - T + r
+ * and sees rows 0..p, itself and everything before it.  Each row is
+ * therefore Algorithm 1 on the prefix of n_r = p + 1 rows (none if p < 0,
+ * giving the zero vector like an empty cache).
+ *   q   [B][h_q][T][d_k]
+ *   out [B][h_q][T][d_v] (fp64)
+ * Returns 0, or -1 on a shape error or an allocation failure.
+ */
+int oracle_decode_multi(const float *q, const float *K, const float *V,
+                        const int32_t *len, float scale, double *out, int B,
+                        int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
+                        int threads)
+{
+    if (B < 1 || h_q < 1 || h_kv < 1 || n_max < 1 || d_k < 1 || d_v < 1 || T < 1)
+        return -1;
+    if (h_q % h_kv != 0) return -1;
+
+    const double sc = (double)scale;
+    int failed = 0;
+    const int64_t units = (int64_t)B * h_q * T;
+
+#ifdef _OPENMP
+    if (threads <= 0) threads = omp_get_max_threads();
+#pragma omp parallel num_threads(threads) reduction(| : failed)
+#endif
+    {
+        double *s = (double *)malloc(sizeof(double) * (size_t)n_max);
+        double *e = (double *)malloc(sizeof(double) * (size_t)n_max);
+        if (!s || !e) failed = 1;
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (int64_t u = 0; u < units; ++u) {
+            if (!s || !e) continue;
+            const int r = (int)(u % T);
+            const int64_t bh = u / T;
+            const int b = (int)(bh / h_q);
+            const int h = (int)(bh % h_q);
+            const int g = kv_head_of(h, h_q, h_kv);
+            /* position of query row r; it sees rows 0..pos */
+            const int64_t pos = rows_used(len[b], n_max) - T + r;
+            const int64_t n = pos >= 0 ? pos + 1 : 0;
+            const float *qv = q + u * d_k;
+            const float *Ks = K + ((int64_t)b * h_kv + g) * n_max * d_k;
+            const float *Vs = V + ((int64_t)b * h_kv + g) * n_max * d_v;
+            decode_one_query(qv, Ks, Vs, n, d_k, d_v, sc, out + u * d_v, s, e,
+                             NULL);
+        }
+        free(s);
+        free(e);
+    }
+    (void)threads;
+    return failed ? -1 : 0;
+}
+
+/*
+ * T rows appended in order: the single-row append above applied T times,
+ * row r of every (b, g) taken from k_new[b][g][r] / v_new[b][g][r].  Each
+ * application writes at the current len[b] and increments it, and does
+ * nothing once the cache is full, so a sequence with room for fewer than T
+ * rows keeps the first ones that fit.
+ *   k_new [B][h_kv][T][d_k], v_new [B][h_kv][T][d_v]
+ */
+int oracle_append_rows(float *K, float *V, const float *k_new,
+                       const float *v_new, int32_t *len, int B, int h_kv,
+                       int n_max, int d_k, int d_v, int T)
+{
+    if (B < 1 || h_kv < 1 || n_max < 1 || d_k < 1 || d_v < 1 || T < 1) return -1;
+    for (int r = 0; r < T; ++r) {
+        for (int b = 0; b < B; ++b) {
+            const int32_t t = len[b];
+            if (t < 0 || t >= n_max) continue;
+            for (int g = 0; g < h_kv; ++g) {
+                const int64_t src = ((int64_t)b * h_kv + g) * T + r;
+                float *Ks = K + ((int64_t)b * h_kv + g) * n_max * d_k;
+                float *Vs = V + ((int64_t)b * h_kv + g) * n_max * d_v;
+                memcpy(Ks + (int64_t)t * d_k, k_new + src * d_k,
+                       sizeof(float) * (size_t)d_k);
+                memcpy(Vs + (int64_t)t * d_v, v_new + src * d_v,
+                       sizeof(float) * (size_t)d_v);
+            }
+            len[b] = t + 1;
+        }
     }
     return 0;
 }

@@ -14,6 +14,7 @@ import pytest
 import oracle
 import test_oracle_bruteforce as bf
 import test_oracle_invariants as inv
+import test_oracle_multi as multi
 import test_oracle_pins as pins
 import test_oracle_vs_sdpa as sdpa
 
@@ -33,9 +34,18 @@ MUTANTS = {
                       "if (len_b > n_max) return n_max;\n    return len_b > 0 ? len_b - 1 : 0;"),
     "one_row_long": ("if (len_b > n_max) return n_max;\n    return len_b;",
                      "if (len_b >= n_max) return n_max;\n    return len_b + 1;"),
-    "append_no_increment": ("len[b] = t + 1;", "(void)0;"),
-    "append_wrong_row": ("memcpy(Ks + (int64_t)t * d_k,", "memcpy(Ks + (int64_t)(t > 0 ? t - 1 : 0) * d_k,"),
+    "append_no_increment": ("        len[b] = t + 1;\n    }\n    return 0;",
+                            "        (void)0;\n    }\n    return 0;"),
+    "append_wrong_row": ("memcpy(Ks + (int64_t)t * d_k, k_new + ((int64_t)b * h_kv + g) * d_k,",
+                         "memcpy(Ks + (int64_t)(t > 0 ? t - 1 : 0) * d_k, k_new + ((int64_t)b * h_kv + g) * d_k,"),
     "max_not_subtracted_wrongly": ("if (s[l] > m) m = s[l];", "if (s[l] < m || m == -INFINITY) m = s[l];\n        m = 0.0;"),
+    "multi_sees_next_row": ("const int64_t pos = rows_used(len[b], n_max) - T + r;",
+                            "const int64_t pos = rows_used(len[b], n_max) - T + r + 1;"),
+    "multi_rows_reversed": ("const int64_t pos = rows_used(len[b], n_max) - T + r;",
+                            "const int64_t pos = rows_used(len[b], n_max) - 1 - r;"),
+    "multi_query_stride": ("const float *qv = q + u * d_k;", "const float *qv = q + bh * d_k;"),
+    "append_rows_reversed": ("const int64_t src = ((int64_t)b * h_kv + g) * T + r;",
+                             "const int64_t src = ((int64_t)b * h_kv + g) * T + (T - 1 - r);"),
 }
 
 
@@ -55,6 +65,9 @@ def _battery():
         inv.test_single_row_returns_that_row_exactly,
         inv.test_append_then_decode_equals_decode_on_full_cache,
         lambda: sdpa.test_table3_multistep_kv_cache_vs_causal_sdpa({"T": 4, "d": 8}),
+        lambda: multi.test_longer_cache_equals_masked_sdpa(4, [37, 9]),
+        multi.test_equals_t_single_steps_bit_for_bit,
+        multi.test_append_rows_offsets_and_capacity,
     ]
     failed = []
     for i, c in enumerate(checks):
