@@ -91,12 +91,16 @@ def cpu_baseline(inp, budget_s: float, step_bytes):
     while True:
         t = done % steps
         t0 = time.perf_counter()
-        if s.steps:
-            oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
-            q = inp.q_step[t]
+        if s.rows > 1:
+            oracle.append_rows(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+            oracle.decode_multi(inp.q_step[t], hK, hV, hl, s.scale32(), threads=threads)
         else:
-            q = inp.q
-        oracle.decode(q, hK, hV, hl, s.scale32(), threads=threads)
+            if s.steps:
+                oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+                q = inp.q_step[t]
+            else:
+                q = inp.q
+            oracle.decode(q, hK, hV, hl, s.scale32(), threads=threads)
         elapsed += time.perf_counter() - t0
         nbytes += step_bytes(hl, bool(s.steps))
         done += 1
@@ -108,8 +112,8 @@ def cpu_baseline(inp, budget_s: float, step_bytes):
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"{done} full step(s) (append + decode of all {s.B * s.h_q} query "
-                   f"heads) of the same workload, {elapsed:.2f} s, fp64 oracle, "
+        "sample": (f"{done} full step(s) (append + decode of all {s.B * s.h_q * s.rows} "
+                   f"query rows) of the same workload, {elapsed:.2f} s, fp64 oracle, "
                    f"{threads} OpenMP threads"),
         "seconds_per_step": elapsed / done,
         "cpu_model": _cpu_model(),
@@ -184,9 +188,15 @@ def main() -> int:
         dq = torch.from_numpy(inp.q_step).to(dev)
     else:
         dq = torch.from_numpy(inp.q[None]).to(dev)
-    out = torch.empty((s.B, s.h_q, s.d_v), dtype=torch.float32, device=dev)
-    chunk = args.chunk_rows or binding.chunk_rows(s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v)
-    ws = binding.alloc_workspace(dq[0], dK, dV, chunk)
+    multi = s.rows > 1
+    out = torch.empty((s.B, s.h_q) + ((s.rows,) if multi else ()) + (s.d_v,),
+                      dtype=torch.float32, device=dev)
+    chunk = args.chunk_rows or binding.chunk_rows(s.B, s.h_q * s.rows, s.h_kv, s.n_max,
+                                                  s.d_k, s.d_v)
+    if multi:
+        ws = binding.alloc_multi_workspace(dq[0], dK, dV, chunk)
+    else:
+        ws = binding.alloc_workspace(dq[0], dK, dV, chunk)
     scale = float(s.scale32())
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -201,6 +211,14 @@ def main() -> int:
             dl.copy_(lens0)              # a new pass over the multi-step sequence
         if ev_a is not None:
             ev_a.record(st)
+        if multi:
+            # several positions per step: da_decode_multi_step, both launches
+            # inside the events
+            binding.decode_multi_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=out,
+                                      workspace=ws, chunk_rows=chunk, stream=st)
+            if ev_b is not None:
+                ev_b.record(st)
+            return
         if s.steps:
             binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk,
                                    k_new=dkn[t], v_new=dvn[t], stream=st)
@@ -226,7 +244,7 @@ def main() -> int:
         if s.steps:
             if t == 0 and i > 0:
                 lens_host = inp.lens.astype(np.int64)
-            lens_host = np.minimum(lens_host + 1, s.n_max)
+            lens_host = np.minimum(lens_host + s.rows, s.n_max)
         step_lens.append(lens_host.copy())
 
     start = torch.cuda.Event(enable_timing=True)
@@ -267,16 +285,19 @@ def main() -> int:
         launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
 
     def step_bytes(lens, with_append=True):
-        b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v)
+        b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v, s.rows)
         if with_append:
-            b += traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v)
+            b += traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v, s.rows)
         return b
 
     alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
     # The partial kernel of a step also writes the appended rows (Prop. 2).
-    append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v) if s.steps else 0
-    launch_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
-                    for l in step_lens]
+    append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v, s.rows) if s.steps else 0
+    if multi:   # the events hold the whole step (partial + merge)
+        launch_bytes = [step_bytes(l) for l in step_lens]
+    else:
+        launch_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
+                        for l in step_lens]
     ms_per_step = total_ms / args.steps
     value = alg_bytes / (total_ms * 1e-3) / 1e9
     launch_avg_ms = sum(launch_ms) / len(launch_ms)
@@ -301,8 +322,11 @@ def main() -> int:
             "n_max": s.n_max,
             "initial_len": [int(x) for x in inp.lens],
             "steps_per_sequence": s.steps,
+            "rows_per_step": s.rows,
             "chunk_rows": chunk,
-            "step": ("decode_partial with fused kv_append + decode_merge" if s.steps
+            "step": ("da_decode_multi_step (T-row append fused, causal T-row decode)"
+                     if multi else
+                     "decode_partial with fused kv_append + decode_merge" if s.steps
                      else "decode_partial + decode_merge"),
             "graph": bool(args.graph),
         },
@@ -312,14 +336,16 @@ def main() -> int:
         "host_wall_s": round(wall, 4),
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode_partial_kernel",
+            "kernel": ("decode_partial_kernel + decode_merge_kernel (the whole step)"
+                       if multi else "decode_partial_kernel"),
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": counter_traffic(s.name),
+            "traffic": None if multi else counter_traffic(s.name),
             "avg_launch_us": round(launch_avg_ms * 1e3, 2),
             "timing": ("graph replay / steps (partial + merge)" if args.graph
+                       else "HIP events around each step (partial + merge)" if multi
                        else "HIP events around each partial launch"),
             "algorithmic_bytes_per_launch": int(sum(launch_bytes) / len(launch_bytes)),
         },

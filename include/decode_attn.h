@@ -180,6 +180,44 @@ da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
                           void *stream);
 
 /*
+ * Decode with T query rows per query head (T >= 1): the rank-2 query of the
+ * paper's training form, softmax(scale * Q (+.x Omega<2,2>) K)
+ * (+.x Omega<2,2>) V, for a step that submits T consecutive positions at
+ * once (speculative verification, chunked prefill), with causal visibility:
+ * query row r of sequence b sits at cache position p = clamp(len[b], 0,
+ * n_max) - T + r and attends rows 0..p; a row with p < 0 gives 0.  T = 1 is
+ * da_decode_attn.
+ *     q   float [B][h_q][T][d_k]      out float [B][h_q][T][d_v]
+ * The T rows of every query head of a group are scored from the same K/V
+ * reads (the kernels treat them as h_q*T query heads), so the workspace is
+ * that of a single-row decode with h_q*T query heads:
+ * da_decode_workspace_bytes(B, h_q*T, h_kv, ...) bytes, its counter region
+ * da_decode_workspace_counter_bytes(B, h_q*T, h_kv, ...).  T <= 4096.  Other
+ * rules as da_decode_attn.
+ */
+da_status da_decode_multi(const float *q, const float *K, const float *V,
+                          const int32_t *len, float scale, float *out, int B,
+                          int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
+                          int chunk_rows, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/*
+ * T autoregressive steps in one: the effect of T successive da_decode_step
+ * calls whose rows are given together -- row r of k_new [B][h_kv][T][d_k] /
+ * v_new [B][h_kv][T][d_v] appended at len[b] + r while the cache has room
+ * (da_kv_append_rows), and query row r of q [B][h_q][T][d_k] attending rows
+ * 0 .. min(len[b] + r, n_max - 1) of the grown cache (len[b] the value on
+ * entry; nothing if len[b] < 0).  Two launches; len advances by the rows
+ * that fit.  Workspace as da_decode_multi.
+ */
+da_status da_decode_multi_step(const float *q, float *K, float *V,
+                               const float *k_new, const float *v_new,
+                               int32_t *len, float scale, float *out, int B,
+                               int h_q, int h_kv, int n_max, int d_k, int d_v,
+                               int T, int chunk_rows, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
+/*
  * KV-cache append, eqs. (6)-(7) (K_{t+1} = K_t # k_t, V_{t+1} = V_t # v_t,
  * Proposition 2): for every b with 0 <= t = len[b] < n_max and every KV head
  * g, copies k_new[b,g,:] to K[b,g,t,:] and v_new[b,g,:] to V[b,g,t,:] bit for
@@ -191,6 +229,16 @@ da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
 da_status da_kv_append(float *K, float *V, const float *k_new,
                        const float *v_new, int32_t *len, int B, int h_kv,
                        int n_max, int d_k, int d_v, void *stream);
+
+/*
+ * T rows at once: da_kv_append applied T times in order, row r of every
+ * (b, g) taken from k_new [B][h_kv][T][d_k] / v_new [B][h_kv][T][d_v].  Rows
+ * land at len[b] + r while the cache has room; len[b] advances by the rows
+ * written.  1 <= T <= 4096; other rules as da_kv_append.
+ */
+da_status da_kv_append_rows(float *K, float *V, const float *k_new,
+                            const float *v_new, int32_t *len, int B, int h_kv,
+                            int n_max, int d_k, int d_v, int T, void *stream);
 
 #ifdef __cplusplus
 }

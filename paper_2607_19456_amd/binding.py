@@ -35,6 +35,9 @@ SIGNATURES = {
     "da_decode_partial": (_ci, [_vp] * 6 + [_cf] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
+    "da_decode_multi": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
+    "da_decode_multi_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
+    "da_kv_append_rows": (_ci, [_vp] * 5 + [_ci] * 6 + [_vp]),
 }
 
 
@@ -212,3 +215,80 @@ def kv_append(K, V, k_new, v_new, lens, stream=None) -> None:
         _dev(K, "K", torch.float32), _dev(V, "V", torch.float32),
         _dev(k_new, "k_new", torch.float32), _dev(v_new, "v_new", torch.float32),
         _dev(lens, "len", torch.int32), B, h_kv, n_max, d_k, d_v, _stream(stream)))
+
+
+# --- several query rows per head (causal) -------------------------------------
+
+def _multi_shapes(q, K, V):
+    if q.dim() != 4 or K.dim() != 4 or V.dim() != 4:
+        raise ValueError("q must be [B,h_q,T,d_k], K [B,h_kv,n_max,d_k], V [B,h_kv,n_max,d_v]")
+    B, h_q, T, d_k = q.shape
+    Bk, h_kv, n_max, d_k2 = K.shape
+    Bv, h_kv2, n_max2, d_v = V.shape
+    if not (B == Bk == Bv and h_kv == h_kv2 and n_max == n_max2 and d_k == d_k2):
+        raise ValueError("inconsistent q/K/V shapes")
+    return B, h_q, h_kv, n_max, d_k, d_v, T
+
+
+def alloc_multi_workspace(q, K, V, chunk_rows: int = 0) -> torch.Tensor:
+    """A zeroed workspace for multi-row decodes of these shapes (q [B,h_q,T,d_k])."""
+    B, h_q, h_kv, n_max, d_k, d_v, T = _multi_shapes(q, K, V)
+    n = workspace_bytes(B, h_q * T, h_kv, n_max, d_k, d_v, chunk_rows)
+    if n == 0:
+        _check("da_decode_workspace_bytes", 2)
+    return torch.zeros(n, dtype=torch.uint8, device=q.device)
+
+
+def decode_multi(q, K, V, lens, scale: float, out=None, workspace=None,
+                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
+    """T query rows per head, causal: row r of sequence b attends cache rows
+    0 .. len[b]-T+r.  q [B,h_q,T,d_k] -> out [B,h_q,T,d_v]."""
+    B, h_q, h_kv, n_max, d_k, d_v, T = _multi_shapes(q, K, V)
+    if out is None:
+        out = torch.empty((B, h_q, T, d_v), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_multi_workspace(q, K, V, chunk_rows)
+    wp, wn = _ws(workspace)
+    _check("da_decode_multi", _lib.da_decode_multi(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
+        d_v, T, int(chunk_rows), wp, wn, _stream(stream)))
+    return out
+
+
+def decode_multi_step(q, K, V, k_new, v_new, lens, scale: float, out=None,
+                      workspace=None, chunk_rows: int = 0, stream=None) -> torch.Tensor:
+    """T successive decode steps at once: append k_new/v_new [B,h_kv,T,d] at
+    len[b].., then query row r attends rows 0 .. len[b]+r (len on entry)."""
+    B, h_q, h_kv, n_max, d_k, d_v, T = _multi_shapes(q, K, V)
+    if tuple(k_new.shape) != (B, h_kv, T, d_k) or tuple(v_new.shape) != (B, h_kv, T, d_v):
+        raise ValueError("k_new must be [B,h_kv,T,d_k] and v_new [B,h_kv,T,d_v]")
+    if out is None:
+        out = torch.empty((B, h_q, T, d_v), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_multi_workspace(q, K, V, chunk_rows)
+    wp, wn = _ws(workspace)
+    _check("da_decode_multi_step", _lib.da_decode_multi_step(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(k_new, "k_new", torch.float32),
+        _dev(v_new, "v_new", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
+        d_v, T, int(chunk_rows), wp, wn, _stream(stream)))
+    return out
+
+
+def kv_append_rows(K, V, k_new, v_new, lens, stream=None) -> None:
+    """Append T rows per KV head (k_new [B,h_kv,T,d_k]) at len[b].., as many
+    as fit; len[b] advances by the rows written."""
+    if K.dim() != 4 or V.dim() != 4 or k_new.dim() != 4:
+        raise ValueError("K, V must be [B,h_kv,n_max,d] and k_new/v_new [B,h_kv,T,d]")
+    B, h_kv, n_max, d_k = K.shape
+    d_v = V.shape[3]
+    T = k_new.shape[2]
+    if tuple(k_new.shape) != (B, h_kv, T, d_k) or tuple(v_new.shape) != (B, h_kv, T, d_v):
+        raise ValueError("k_new must be [B,h_kv,T,d_k] and v_new [B,h_kv,T,d_v]")
+    _check("da_kv_append_rows", _lib.da_kv_append_rows(
+        _dev(K, "K", torch.float32), _dev(V, "V", torch.float32),
+        _dev(k_new, "k_new", torch.float32), _dev(v_new, "v_new", torch.float32),
+        _dev(lens, "len", torch.int32), B, h_kv, n_max, d_k, d_v, T, _stream(stream)))

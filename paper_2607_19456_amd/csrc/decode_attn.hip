@@ -68,6 +68,7 @@ constexpr int kDefaultChunkRows = 768;
 // Visit slots per slab, in units of the even share of waves per slab.
 constexpr int kVisitSlack = 4;
 constexpr int64_t kMaxSlabs = 1 << 20;
+constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
 // Each slab's scheduling word, {chunks taken (low half), visits opened (high
 // half)}, has a 128-byte line of its own, so atomics on different slabs'
 // words never serialize on the same line.
@@ -122,49 +123,61 @@ __device__ __forceinline__ int rows_used(int32_t len_b, int n_max) {
   return len_b < 0 ? 0 : (len_b > n_max ? n_max : len_b);
 }
 
-// With a fused append, the decode of sequence b also covers row len[b] (the
-// appended one) when the cache has room for it.
+// With a fused append of T rows, the decode of sequence b also covers the
+// appended rows len[b] .. len[b]+T-1 that fit in the cache.
 __device__ __forceinline__ bool appends(bool app, int32_t len_b, int n_max) {
   return app && len_b >= 0 && len_b < n_max;
 }
 
-__device__ __forceinline__ int decode_rows(int32_t len_b, int n_max, bool app) {
-  return appends(app, len_b, n_max) ? len_b + 1 : rows_used(len_b, n_max);
+__device__ __forceinline__ int appended_rows(bool app, int32_t len_b, int n_max, int T) {
+  return appends(app, len_b, n_max) ? min(T, n_max - len_b) : 0;
+}
+
+__device__ __forceinline__ int decode_rows(int32_t len_b, int n_max, bool app, int T) {
+  return appends(app, len_b, n_max) ? len_b + appended_rows(app, len_b, n_max, T)
+                                    : rows_used(len_b, n_max);
 }
 
 // ---------------------------------------------------------------------------
-// KV append.  One workgroup per sequence; every thread reads len[b] before
-// the barrier, thread 0 writes it after, so no thread can see the new value.
+// KV append of T rows.  One workgroup per sequence; every thread reads len[b]
+// before the barrier, thread 0 writes it after, so no thread can see the new
+// value.  Rows r = 0..T-1 land at len[b] + r as long as they fit (the
+// single-row append applied T times).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(
     float* __restrict__ K, float* __restrict__ V,
     const float* __restrict__ k_new, const float* __restrict__ v_new,
-    int32_t* __restrict__ len, int h_kv, int n_max, int d_k, int d_v) {
+    int32_t* __restrict__ len, int h_kv, int n_max, int d_k, int d_v, int T) {
   const int b = blockIdx.x;
   const int32_t t = len[b];
-  const bool room = t >= 0 && t < n_max;
-  if (room) {
+  const int cnt = (t >= 0 && t < n_max) ? min(T, n_max - t) : 0;
+  if (cnt > 0) {
     const int ck = d_k / 4, cv = d_v / 4;            // 16-byte chunks per row
-    const int per_head = ck + cv;
+    const int per_row = ck + cv;
+    const int per_head = cnt * per_row;
     const int total = h_kv * per_head;
     for (int c = threadIdx.x; c < total; c += blockDim.x) {
       const int g = c / per_head;
-      const int w = c - g * per_head;
+      const int rem = c - g * per_head;
+      const int r = rem / per_row;
+      const int w = rem - r * per_row;
       const int64_t slab = (int64_t)b * h_kv + g;
+      const int64_t src_row = slab * T + r;
+      const int64_t dst_row = slab * n_max + t + r;
       if (w < ck) {
-        const u4* src = reinterpret_cast<const u4*>(k_new + slab * d_k) + w;
-        u4* dst = reinterpret_cast<u4*>(K + (slab * n_max + t) * d_k) + w;
+        const u4* src = reinterpret_cast<const u4*>(k_new + src_row * d_k) + w;
+        u4* dst = reinterpret_cast<u4*>(K + dst_row * d_k) + w;
         *dst = *src;
       } else {
         const int wv = w - ck;
-        const u4* src = reinterpret_cast<const u4*>(v_new + slab * d_v) + wv;
-        u4* dst = reinterpret_cast<u4*>(V + (slab * n_max + t) * d_v) + wv;
+        const u4* src = reinterpret_cast<const u4*>(v_new + src_row * d_v) + wv;
+        u4* dst = reinterpret_cast<u4*>(V + dst_row * d_v) + wv;
         *dst = *src;
       }
     }
   }
   __syncthreads();
-  if (room && threadIdx.x == 0) len[b] = t + 1;
+  if (cnt > 0 && threadIdx.x == 0) len[b] = t + cnt;
 }
 
 // ---------------------------------------------------------------------------
@@ -176,21 +189,26 @@ struct Tile {
   f4 v[4][DV / 64];       // V rows: lane (i,k) holds row 4k+rho, dims 64c+4i..+3
 };
 
-// Where a tile's rows live: the slab, except row `new_row` (the row a fused
-// append adds; -1 if none), which is read from the incoming k_new / v_new rows.
-// Rows [0, fast_end) are plain slab rows.
+// Where a tile's rows live: the slab, except rows new_lo .. new_lo+new_cnt-1
+// (the rows a fused append adds; new_cnt = 0 if none), which are read from the
+// incoming k_new / v_new rows.  new_row is new_lo when exactly one row is
+// added, else -1.  Rows [0, fast_end) are plain slab rows.
 struct RowSource {
   const float* __restrict__ Ks;
   const float* __restrict__ Vs;
-  const float* __restrict__ k_new_row;
-  const float* __restrict__ v_new_row;
+  const float* __restrict__ k_new_rows;
+  const float* __restrict__ v_new_rows;
+  int new_lo;
+  int new_cnt;
   int new_row;
   int fast_end;
   uint32_t k_lane;          // byte offset of lane (i,k) in a K tile: i*d_k + 4k floats
   uint32_t v_lane;          // byte offset of lane (i,k) in a V tile: 4k*d_v + 4i floats
 };
 
-template <int DK, int DV, int NB>
+// ROWS: a fused append may add several rows (multi-row steps); otherwise at
+// most one, which keeps the redirect a single comparison.
+template <int DK, int DV, int NB, bool ROWS>
 __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& src,
                                           int row0, int last_row, int i, int k) {
   if (row0 + kTileRows <= src.fast_end) {
@@ -209,16 +227,28 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
         T.v[rho][c] = load4_stream(reinterpret_cast<const float*>(vb + src.v_lane) + rho * DV + 64 * c);
     return;
   }
-  // The slab's last tile: rows past the end clamp to the last row, and the
-  // row a fused append adds comes from k_new / v_new.
+  // The slab's last tile(s): rows past the end clamp to the last row, and
+  // the rows a fused append adds come from k_new / v_new.
   const int rk = min(row0 + i, last_row);
-  const float* kp = rk == src.new_row ? src.k_new_row : src.Ks + (int64_t)rk * DK;
+  const float* kp;
+  if constexpr (ROWS)
+    kp = (unsigned)(rk - src.new_lo) < (unsigned)src.new_cnt
+             ? src.k_new_rows + (rk - src.new_lo) * DK
+             : src.Ks + (int64_t)rk * DK;
+  else
+    kp = rk == src.new_row ? src.k_new_rows : src.Ks + (int64_t)rk * DK;
 #pragma unroll
   for (int t = 0; t < DK / 16; ++t) T.k[t] = load4(kp + 16 * t + 4 * k);
 #pragma unroll
   for (int rho = 0; rho < 4; ++rho) {
     const int rv = min(row0 + 4 * k + rho, last_row);
-    const float* vp = rv == src.new_row ? src.v_new_row : src.Vs + (int64_t)rv * DV;
+    const float* vp;
+    if constexpr (ROWS)
+      vp = (unsigned)(rv - src.new_lo) < (unsigned)src.new_cnt
+               ? src.v_new_rows + (rv - src.new_lo) * DV
+               : src.Vs + (int64_t)rv * DV;
+    else
+      vp = rv == src.new_row ? src.v_new_rows : src.Vs + (int64_t)rv * DV;
 #pragma unroll
     for (int c = 0; c < DV / 64; ++c) T.v[rho][c] = load4_stream(vp + 64 * c + 4 * i);
   }
@@ -226,9 +256,9 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
 
 // One 16-row tile for NB column blocks of query heads: scores on the matrix
 // cores, online softmax update, weighted-sum update on the matrix cores.
-template <int DK, int DV, int NB>
-__device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0, int last_row,
-                                             int k, int lane,
+template <int DK, int DV, int NB, bool CAUSAL>
+__device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0,
+                                             const int (&lim)[NB], int k, int lane,
                                              const f4 (*__restrict__ sh_q)[DK / 16][kWave],
                                              float (&m_run)[NB], float (&l_run)[NB],
                                              f4 (&acc)[NB][DV / 64][4]) {
@@ -256,20 +286,24 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
       s1 = mfma_16x16x4(T.k[t + 1].w, qb[t + 1].w, s1);
     }
     f4 s = s0 + s1;
-    // Rows past the split's end take no weight.
+    // Rows past the last row this lane's column sees take no weight.
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      if (row0 + 4 * k + r > last_row) s[r] = -INFINITY;
+      if (row0 + 4 * k + r > lim[nb]) s[r] = -INFINITY;
 
     // Step II, online: running max over the 4 row groups of head i.
     const float tmax = max_over_row_groups(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
     const float m_new = fmaxf(m_run[nb], tmax);
-    const float alpha = fast_exp2(m_run[nb] - m_new);
+    // A causal column may have seen no row yet (m_new = -inf): exponentiate
+    // against 0 then, so every weight is 0 instead of NaN.
+    float m_ref = m_new;
+    if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run[nb] - m_ref);
     f4 pr;
-    pr[0] = fast_exp2(s[0] - m_new);
-    pr[1] = fast_exp2(s[1] - m_new);
-    pr[2] = fast_exp2(s[2] - m_new);
-    pr[3] = fast_exp2(s[3] - m_new);
+    pr[0] = fast_exp2(s[0] - m_ref);
+    pr[1] = fast_exp2(s[1] - m_ref);
+    pr[2] = fast_exp2(s[2] - m_ref);
+    pr[3] = fast_exp2(s[3] - m_ref);
     l_run[nb] = l_run[nb] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
     m_run[nb] = m_new;
     // Once the running maxima settle, most tiles leave them unchanged
@@ -296,8 +330,8 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
 
 // Number of cache rows of slab s = (b, KV head, head group).
 __device__ __forceinline__ int slab_rows(const int32_t* __restrict__ len, int s, int per_b,
-                                         int n_max, bool app) {
-  return decode_rows(len[s / per_b], n_max, app);
+                                         int n_max, bool app, int T) {
+  return decode_rows(len[s / per_b], n_max, app, T);
 }
 
 __device__ __forceinline__ unsigned long long load_word(const unsigned long long* p) {
@@ -310,7 +344,7 @@ __device__ __forceinline__ unsigned long long load_word(const unsigned long long
 // slabs examined up to and including the one returned.
 __device__ int find_open_slab(const unsigned* __restrict__ cnt,
                               const int32_t* __restrict__ len, int start, int budget, int S,
-                              int per_b, int n_max, bool app, int C, int J, int lane,
+                              int per_b, int n_max, bool app, int T, int C, int J, int lane,
                               int* seen) {
   for (int base = 0; base < budget; base += kWave) {
     const int o = base + lane;
@@ -318,7 +352,7 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
     if (sl >= S) sl -= S;
     bool open = false;
     if (o < budget) {
-      const int nch = (slab_rows(len, sl, per_b, n_max, app) + C - 1) / C;
+      const int nch = (slab_rows(len, sl, per_b, n_max, app, T) + C - 1) / C;
       const unsigned long long w = load_word(
           reinterpret_cast<const unsigned long long*>(cnt + (size_t)sl * kCounterStride));
       open = (unsigned)w < (unsigned)nch && (unsigned)(w >> 32) < (unsigned)J;
@@ -359,12 +393,12 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum)
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
 // ---------------------------------------------------------------------------
-template <int DK, int DV, int NB>
+template <int DK, int DV, int NB, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_kernel(
     const float* __restrict__ q, float* __restrict__ K,
     float* __restrict__ V, const float* __restrict__ k_new,
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
-    int B, int h_q, int h_kv, int n_max, int C, int head_groups, int J,
+    int B, int h_q, int h_kv, int n_max, int T, int C, int head_groups, int J,
     unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
     float* __restrict__ ws_acc) {
   const int per_b = h_kv * head_groups;
@@ -386,24 +420,28 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
   __shared__ float sh_m[kWaves - 1][NB][kWave];
   __shared__ float sh_l[kWaves - 1][NB][kWave];
 
-  // Fused append: the workgroups share the row copies -- row len[b] of every
-  // KV head <- k_new / v_new, bit for bit.  The decode below never reads
-  // that row from the cache (it takes it straight from k_new / v_new), so no
-  // ordering between the copies and the reads is needed; len[b] itself is
-  // only advanced by the merge, after every workgroup has read it.
+  // Fused append: the workgroups share the row copies -- rows len[b] + r of
+  // every KV head <- k_new / v_new row r (those that fit), bit for bit.  The
+  // decode below never reads those rows from the cache (it takes them
+  // straight from k_new / v_new), so no ordering between the copies and the
+  // reads is needed; len[b] itself is only advanced by the merge, after every
+  // workgroup has read it.
   if (app) {
     constexpr int ck = DK / 4, cv = DV / 4;             // 16-byte chunks per row
     for (int u = blockIdx.x; u < B * h_kv; u += gridDim.x) {
       const int b = u / h_kv;
       const int32_t t = len[b];
-      if (t < 0 || t >= n_max) continue;
-      const int64_t row = (int64_t)u * n_max + t;
-      for (int w = tid; w < ck + cv; w += kThreads) {
-        if (w < ck)
-          reinterpret_cast<u4*>(K + row * DK)[w] = reinterpret_cast<const u4*>(k_new + (int64_t)u * DK)[w];
+      const int cnt = appended_rows(app, t, n_max, T);
+      for (int w = tid; w < cnt * (ck + cv); w += kThreads) {
+        const int r = w / (ck + cv);
+        const int x = w - r * (ck + cv);
+        const int64_t row = (int64_t)u * n_max + t + r;
+        const int64_t src = (int64_t)u * T + r;
+        if (x < ck)
+          reinterpret_cast<u4*>(K + row * DK)[x] = reinterpret_cast<const u4*>(k_new + src * DK)[x];
         else
-          reinterpret_cast<u4*>(V + row * DV)[w - ck] =
-              reinterpret_cast<const u4*>(v_new + (int64_t)u * DV)[w - ck];
+          reinterpret_cast<u4*>(V + row * DV)[x - ck] =
+              reinterpret_cast<const u4*>(v_new + src * DV)[x - ck];
       }
     }
   }
@@ -419,12 +457,12 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       int budget = S;
       while (budget > 0) {
         int seen;
-        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, C, J,
+        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, T, C, J,
                                         lane, &seen);
         if (cand < 0) break;
         budget -= seen;
         start = cand + 1 == S ? 0 : cand + 1;
-        const int nch = (slab_rows(len, cand, per_b, n_max, app) + C - 1) / C;
+        const int nch = (slab_rows(len, cand, per_b, n_max, app, T) + C - 1) / C;
         unsigned long long got = ~0ull;
         if (lane == 0) {
           unsigned long long* w =
@@ -462,7 +500,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     const int g = rem / head_groups;
     const int hgrp = rem - g * head_groups;
     const int32_t len_b = len[b];
-    const int n = decode_rows(len_b, n_max, app);
+    const int n = decode_rows(len_b, n_max, app, T);
     const int nch = (n + C - 1) / C;
     const int last_row = n - 1;
     const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
@@ -473,12 +511,29 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     RowSource src;
     src.Ks = K + slab * n_max * DK;
     src.Vs = V + slab * n_max * DV;
-    src.new_row = appends(app, len_b, n_max) ? len_b : -1;
-    src.fast_end = src.new_row >= 0 ? src.new_row : n;
-    src.k_new_row = app ? k_new + slab * DK : nullptr;
-    src.v_new_row = app ? v_new + slab * DV : nullptr;
+    src.new_cnt = appended_rows(app, len_b, n_max, T);
+    src.new_lo = src.new_cnt > 0 ? len_b : n;
+    src.new_row = src.new_cnt == 1 ? len_b : -1;
+    src.fast_end = src.new_lo;
+    src.k_new_rows = app ? k_new + slab * T * DK : nullptr;
+    src.v_new_rows = app ? v_new + slab * T * DV : nullptr;
     src.k_lane = (uint32_t)(i * DK + 4 * k) * sizeof(float);
     src.v_lane = (uint32_t)(4 * k * DV + 4 * i) * sizeof(float);
+
+    // Last row each lane's column sees.  A causal column is query row
+    // r = (its index in the KV head's group) mod T, at position pos0 + r:
+    // pos0 = len[b] before a fused append (the rows of one step enter one per
+    // position), else n - T (the last T positions of the cache).
+    int lim[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      lim[nb] = last_row;
+      if constexpr (CAUSAL) {
+        const int vh = hgrp * (NB * kHeadsPerBlock) + nb * kHeadsPerBlock + i;
+        const int pos0 = app ? (int)len_b : n - T;
+        lim[nb] = (int)std::min<int64_t>((int64_t)pos0 + vh % T, last_row);
+      }
+    }
 
     // B operand of the score product, staged in LDS in register order: entry
     // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
@@ -521,8 +576,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
                                   : last_row);
     };
     Tile<DK, DV, NB> t0, t1, t2;
-    load_tile(t0, src, row_of(0, c, cn), last_row, i, k);
-    if constexpr (kRing<NB> == 3) load_tile(t1, src, row_of(1, c, cn), last_row, i, k);
+    load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(0, c, cn), last_row, i, k);
+    if constexpr (kRing<NB> == 3) load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(1, c, cn), last_row, i, k);
     for (int it = 0;; ++it) {
       // Thread 0 asks for the chunk after next even on the last chunk (the
       // counter simply runs past the end): a conditional request would merge
@@ -539,25 +594,25 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
           const int r0 = row_of(t, c, cn);
           const int r1 = row_of(t + 1, c, cn);
           const int r2 = row_of(t + 2, c, cn);
-          load_tile(t2, src, r2, last_row, i, k);
+          load_tile<DK, DV, NB, CAUSAL>(t2, src, r2, last_row, i, k);
           if (r0 <= last_row)
-            process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t0, src, row_of(t + 3, c, cn), last_row, i, k);
+            process_tile<DK, DV, NB, CAUSAL>(t0, r0, lim, k, lane, sh_q, m_run, l_run, acc);
+          load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(t + 3, c, cn), last_row, i, k);
           if (r1 <= last_row)
-            process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t1, src, row_of(t + 4, c, cn), last_row, i, k);
+            process_tile<DK, DV, NB, CAUSAL>(t1, r1, lim, k, lane, sh_q, m_run, l_run, acc);
+          load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(t + 4, c, cn), last_row, i, k);
           if (r2 <= last_row)
-            process_tile<DK, DV, NB>(t2, r2, last_row, k, lane, sh_q, m_run, l_run, acc);
+            process_tile<DK, DV, NB, CAUSAL>(t2, r2, lim, k, lane, sh_q, m_run, l_run, acc);
           t += 3;
         } else {
           const int r0 = row_of(t, c, cn);
           const int r1 = row_of(t + 1, c, cn);
-          load_tile(t1, src, r1, last_row, i, k);
+          load_tile<DK, DV, NB, CAUSAL>(t1, src, r1, last_row, i, k);
           if (r0 <= last_row)
-            process_tile<DK, DV, NB>(t0, r0, last_row, k, lane, sh_q, m_run, l_run, acc);
-          load_tile(t0, src, row_of(t + 2, c, cn), last_row, i, k);
+            process_tile<DK, DV, NB, CAUSAL>(t0, r0, lim, k, lane, sh_q, m_run, l_run, acc);
+          load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(t + 2, c, cn), last_row, i, k);
           if (r1 <= last_row)
-            process_tile<DK, DV, NB>(t1, r1, last_row, k, lane, sh_q, m_run, l_run, acc);
+            process_tile<DK, DV, NB, CAUSAL>(t1, r1, lim, k, lane, sh_q, m_run, l_run, acc);
           t += 2;
         }
       } while (t < tpw);
@@ -592,12 +647,15 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     if (wave == 0) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        // Wave 0 always holds the visit's first row, so M is finite; a wave
-        // that saw no row has m = -inf and weight exp2(-inf) = 0.
+        // Wave 0 always holds the visit's first row, so M is finite (unless
+        // a causal column sees none of the visit's rows); a wave that saw no
+        // row has m = -inf and weight exp2(-inf) = 0.
         float M = m_run[nb];
 #pragma unroll
         for (int w = 0; w < kWaves - 1; ++w) M = fmaxf(M, sh_m[w][nb][lane]);
-        const float w0 = fast_exp2(m_run[nb] - M);
+        float M_ref = M;
+        if constexpr (CAUSAL) M_ref = M == -INFINITY ? 0.f : M;
+        const float w0 = fast_exp2(m_run[nb] - M_ref);
         float L = l_run[nb] * w0;
 #pragma unroll
         for (int cc = 0; cc < DV / 64; ++cc)
@@ -605,7 +663,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
           for (int e = 0; e < 4; ++e) acc[nb][cc][e] *= w0;
 #pragma unroll
         for (int w = 0; w < kWaves - 1; ++w) {
-          const float ww = fast_exp2(sh_m[w][nb][lane] - M);
+          const float ww = fast_exp2(sh_m[w][nb][lane] - M_ref);
           L += sh_l[w][nb][lane] * ww;
 #pragma unroll
           for (int cc = 0; cc < DV / 64; ++cc)
@@ -653,7 +711,7 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
     float* __restrict__ out, const float2* __restrict__ ws_ml,
     const float* __restrict__ ws_acc, int h_q, int h_kv, int head_groups, int heads_per_group,
     int merge_heads, int J, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis,
-    int32_t* __restrict__ len_bump, int n_max) {
+    int32_t* __restrict__ len_bump, int n_max, int T) {
   constexpr int kCols = DV / 4;                         // 16-byte columns per row
   constexpr int kLanesV = kThreads / kCols;             // visits merged in parallel
   const int s = blockIdx.x / merge_heads;
@@ -716,11 +774,12 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
       // The slab's line: read by no merge workgroup, so its first head's
       // workgroup clears it.
       *reinterpret_cast<unsigned long long*>(cnt + (size_t)s * kCounterStride) = 0ull;
-      // Completing a fused append: len[b] advances once per sequence, after
-      // the partial kernel (which read it) has finished.
+      // Completing a fused append: len[b] advances once per sequence (by
+      // the rows that fit), after the partial kernel (which read it) has
+      // finished.
       if (len_bump && g == 0 && hgrp == 0) {
         const int32_t t = len_bump[b];
-        if (t >= 0 && t < n_max) len_bump[b] = t + 1;
+        if (t >= 0 && t < n_max) len_bump[b] = t + min(T, n_max - t);
       }
     }
   }
@@ -815,36 +874,55 @@ struct PartialArgs {
   const float* v_new;
   const int32_t* len;
   float qscale;
-  int B, h_q, h_kv, n_max;
+  int B, h_q, h_kv, n_max;   // h_q counts query rows: heads x T
+  int T;                     // query rows per head (1: single-query decode)
 };
 
-template <int DK, int DV, int NB>
+template <int DK, int DV, int NB, bool CAUSAL>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB>), dim3(pl.grid), dim3(kThreads), 0,
-                     stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
-                     a.h_kv, a.n_max, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.nvis, w.ml,
-                     w.acc);
+  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL>), dim3(pl.grid), dim3(kThreads),
+                     0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
+                     a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.nvis,
+                     w.ml, w.acc);
 }
 
 template <int DK, int DV>
 void launch_partial_nb(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t s) {
-  if (pl.blocks == 1)
-    launch_partial<DK, DV, 1>(pl, a, w, s);
-  else
-    launch_partial<DK, DV, 2>(pl, a, w, s);
+  if (a.T > 1) {
+    if (pl.blocks == 1)
+      launch_partial<DK, DV, 1, true>(pl, a, w, s);
+    else
+      launch_partial<DK, DV, 2, true>(pl, a, w, s);
+  } else {
+    if (pl.blocks == 1)
+      launch_partial<DK, DV, 1, false>(pl, a, w, s);
+    else
+      launch_partial<DK, DV, 2, false>(pl, a, w, s);
+  }
+}
+
+// Query rows (h_q x T) as the plan's query-head count, or -1 if T is out of
+// range or the product overflows.
+int query_rows(int h_q, int T) {
+  if (T < 1 || T > kMaxQueryRows) return -1;
+  const int64_t r = (int64_t)h_q * T;
+  return r > 2147483647 ? -1 : (int)r;
 }
 
 // Validation of everything but `out` in the documented order (NULL, shapes,
-// alignment, scale, workspace), then the partial launch.
+// alignment, scale, workspace), then the partial launch.  T query rows per
+// head (T > 1: causal), planned as h_q*T query heads.
 da_status partial_impl(const float* q, const float* K, const float* V, const float* k_new,
                        const float* v_new, const int32_t* len, float scale, int B, int h_q,
-                       int h_kv, int n_max, int d_k, int d_v, int chunk_rows, void* workspace,
-                       size_t workspace_bytes, void* stream, const float* out, bool need_out,
-                       Plan* out_plan) {
+                       int h_kv, int n_max, int d_k, int d_v, int T, int chunk_rows,
+                       void* workspace, size_t workspace_bytes, void* stream, const float* out,
+                       bool need_out, Plan* out_plan) {
   if (!q || !K || !V || !len || (need_out && !out)) return DA_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return DA_ERR_NULL;
+  const int rows = query_rows(h_q, T);
+  if (rows < 0 || h_q < 1) return DA_ERR_SHAPE;
   Plan pl;
-  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
+  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4) ||
       !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(out, 16))
@@ -857,7 +935,7 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
   const WsView w = view(pl, workspace);
   // K and V are written only when a fused append is asked for (k_new set).
   const PartialArgs a{q, const_cast<float*>(K), const_cast<float*>(V), k_new, v_new, len,
-                      scale * kLog2e, B, h_q, h_kv, n_max};
+                      scale * kLog2e, B, rows, h_kv, n_max, T};
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, a, w, s);
@@ -868,11 +946,13 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
 }
 
 da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, int n_max,
-                     int d_k, int d_v, int chunk_rows, void* workspace, size_t workspace_bytes,
-                     void* stream) {
+                     int d_k, int d_v, int T, int chunk_rows, void* workspace,
+                     size_t workspace_bytes, void* stream) {
   if (!out) return DA_ERR_NULL;
+  const int rows = query_rows(h_q, T);
+  if (rows < 0 || h_q < 1) return DA_ERR_SHAPE;
   Plan pl;
-  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
+  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
   if (st != DA_OK) return st;
   if (!aligned(out, 16) || !aligned(len_bump, 4)) return DA_ERR_ALIGN;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
@@ -885,12 +965,12 @@ da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, in
   const dim3 grid((unsigned)pl.slabs * (unsigned)pl.merge_heads);
   if (d_v == 64)
     hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
-                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
-                       w.nvis, len_bump, n_max);
+                       rows, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
+                       w.nvis, len_bump, n_max, T);
   else
     hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
-                       h_q, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
-                       w.nvis, len_bump, n_max);
+                       rows, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
+                       w.nvis, len_bump, n_max, T);
   return launch_status();
 }
 
@@ -936,14 +1016,14 @@ da_status da_decode_partial(const float* q, float* K, float* V, const float* k_n
                             const float* v_new, const int32_t* len, float scale, int B,
                             int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
                             void* workspace, size_t workspace_bytes, void* stream) {
-  return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
+  return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v, 1,
                       chunk_rows, workspace, workspace_bytes, stream, nullptr, false, nullptr);
 }
 
 da_status da_decode_merge(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
                           int d_k, int d_v, int chunk_rows, void* workspace,
                           size_t workspace_bytes, void* stream) {
-  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, workspace,
+  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, 1, chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 
@@ -951,43 +1031,67 @@ da_status da_decode_attn(const float* q, const float* K, const float* V, const i
                          float scale, float* out, int B, int h_q, int h_kv, int n_max,
                          int d_k, int d_v, int chunk_rows, void* workspace,
                          size_t workspace_bytes, void* stream) {
-  Plan pl;
-  da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
-                              d_v, chunk_rows, workspace, workspace_bytes, stream, out, true,
-                              &pl);
-  if (st != DA_OK) return st;
-  return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
-                    workspace_bytes, stream);
+  return da_decode_multi(q, K, V, len, scale, out, B, h_q, h_kv, n_max, d_k, d_v, 1,
+                         chunk_rows, workspace, workspace_bytes, stream);
 }
 
 da_status da_decode_step(const float* q, float* K, float* V, const float* k_new,
                          const float* v_new, int32_t* len, float scale, float* out, int B,
                          int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
                          void* workspace, size_t workspace_bytes, void* stream) {
-  if (!k_new || !v_new) return DA_ERR_NULL;
+  return da_decode_multi_step(q, K, V, k_new, v_new, len, scale, out, B, h_q, h_kv, n_max,
+                              d_k, d_v, 1, chunk_rows, workspace, workspace_bytes, stream);
+}
+
+da_status da_decode_multi(const float* q, const float* K, const float* V, const int32_t* len,
+                          float scale, float* out, int B, int h_q, int h_kv, int n_max,
+                          int d_k, int d_v, int T, int chunk_rows, void* workspace,
+                          size_t workspace_bytes, void* stream) {
   Plan pl;
-  da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
-                              chunk_rows, workspace, workspace_bytes, stream, out, true, &pl);
+  da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
+                              d_v, T, chunk_rows, workspace, workspace_bytes, stream, out, true,
+                              &pl);
   if (st != DA_OK) return st;
-  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, pl.chunk_rows, workspace,
+  return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
 }
 
-da_status da_kv_append(float* K, float* V, const float* k_new, const float* v_new,
-                       int32_t* len, int B, int h_kv, int n_max, int d_k, int d_v,
-                       void* stream) {
+da_status da_decode_multi_step(const float* q, float* K, float* V, const float* k_new,
+                               const float* v_new, int32_t* len, float scale, float* out,
+                               int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
+                               int chunk_rows, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  if (!k_new || !v_new) return DA_ERR_NULL;
+  Plan pl;
+  da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
+                              T, chunk_rows, workspace, workspace_bytes, stream, out, true, &pl);
+  if (st != DA_OK) return st;
+  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
+                    workspace_bytes, stream);
+}
+
+da_status da_kv_append_rows(float* K, float* V, const float* k_new, const float* v_new,
+                            int32_t* len, int B, int h_kv, int n_max, int d_k, int d_v, int T,
+                            void* stream) {
   if (!K || !V || !k_new || !v_new || !len) return DA_ERR_NULL;
-  if (B < 1 || h_kv < 1 || n_max < 1 || d_k < 1 || d_v < 1 || B > 2147483647) return DA_ERR_SHAPE;
+  if (B < 1 || h_kv < 1 || n_max < 1 || d_k < 1 || d_v < 1 || T < 1 || T > kMaxQueryRows)
+    return DA_ERR_SHAPE;
   if (d_k % 4 != 0 || d_v % 4 != 0) return DA_ERR_UNSUPPORTED;
-  if ((int64_t)h_kv * (d_k / 4 + d_v / 4) > 2147483647) return DA_ERR_SHAPE;
+  if ((int64_t)h_kv * T * (d_k / 4 + d_v / 4) > 2147483647) return DA_ERR_SHAPE;
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
       !aligned(len, 4))
     return DA_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   hipLaunchKernelGGL(kv_append_kernel, dim3((unsigned)B), dim3(kThreads), 0, s, K, V, k_new,
-                     v_new, len, h_kv, n_max, d_k, d_v);
+                     v_new, len, h_kv, n_max, d_k, d_v, T);
   return launch_status();
+}
+
+da_status da_kv_append(float* K, float* V, const float* k_new, const float* v_new,
+                       int32_t* len, int B, int h_kv, int n_max, int d_k, int d_v,
+                       void* stream) {
+  return da_kv_append_rows(K, V, k_new, v_new, len, B, h_kv, n_max, d_k, d_v, 1, stream);
 }
 
 }  // extern "C"

@@ -59,25 +59,26 @@ def gqa_table(n: int, d_k: int, d_v: int, h_q: int, h_kv: int) -> tuple[int, int
 
 
 def batch_decode_bytes(lens: Iterable[int], h_q: int, h_kv: int, d_k: int,
-                       d_v: int) -> int:
+                       d_v: int, rows: int = 1) -> int:
     """Decode over a batch: every KV head of sequence b read once over its
     len_b rows (Table 6's KV term), plus each query head's q read and output
-    write (Table 6's total)."""
+    write (Table 6's total), for each of ``rows`` query rows per head."""
     lens = [max(0, int(n)) for n in lens]
     kv = sum(h_kv * n * (d_k + d_v) * F32 for n in lens)
-    return kv + len(lens) * h_q * (d_k + d_v) * F32
+    return kv + len(lens) * h_q * rows * (d_k + d_v) * F32
 
 
 def batch_partial_bytes(lens: Iterable[int], h_q: int, h_kv: int, d_k: int,
-                        d_v: int) -> int:
+                        d_v: int, rows: int = 1) -> int:
     """Bytes the split-partial kernel must read: K and V over the valid rows
     of every KV head, and every query vector (the output row is written by
     the merge)."""
     lens = [max(0, int(n)) for n in lens]
     kv = sum(h_kv * n * (d_k + d_v) * F32 for n in lens)
-    return kv + len(lens) * h_q * d_k * F32
+    return kv + len(lens) * h_q * rows * d_k * F32
 
 
-def batch_append_bytes(B: int, h_kv: int, d_k: int, d_v: int) -> int:
-    """Proposition 2 over a batch: one K row and one V row per KV head."""
-    return B * h_kv * append_bytes(d_k, d_v)
+def batch_append_bytes(B: int, h_kv: int, d_k: int, d_v: int, rows: int = 1) -> int:
+    """Proposition 2 over a batch: one K row and one V row per KV head (per
+    appended position)."""
+    return B * h_kv * rows * append_bytes(d_k, d_v)

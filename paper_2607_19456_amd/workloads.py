@@ -119,7 +119,9 @@ class Shape:
 
     ``len_lo``/``len_hi`` bound the initial per-sequence lengths (inclusive);
     ``steps`` is the number of (append, decode) steps (0: one decode of the
-    initial cache, no append)."""
+    initial cache, no append); ``rows`` is the number of positions a step
+    submits at once (query rows per head and rows appended per KV head;
+    1: the single-query decode)."""
     name: str
     B: int
     h_q: int
@@ -132,6 +134,7 @@ class Shape:
     steps: int
     scale: float = field(default=0.0)
     description: str = ""
+    rows: int = 1
 
     @property
     def G(self) -> int:
@@ -165,6 +168,14 @@ WORKLOADS = {
         d_v=128, n_max=131072, len_lo=65536, len_hi=131072 - 64, steps=64,
         description="long-context ragged GQA (group 8), B=4, d=128, "
                     "len ~ U{65536..131008}, n_max=131072, 64 append+decode steps"),
+    # Several positions per step (speculative verification of 4 draft tokens)
+    # on the long-context workload: the same 64 positions in 16 steps.
+    "gqa64x8_b4_d128_ragged64k-128k_16steps_x4rows": Shape(
+        "gqa64x8_b4_d128_ragged64k-128k_16steps_x4rows", B=4, h_q=64, h_kv=8, d_k=128,
+        d_v=128, n_max=131072, len_lo=65536, len_hi=131072 - 64, steps=16, rows=4,
+        description="long-context ragged GQA (group 8), B=4, d=128, "
+                    "len ~ U{65536..131008}, 16 steps of 4 positions each "
+                    "(4 rows appended, 4 causal query rows per head)"),
 }
 
 # Short aliases used on command lines and in test ids.
@@ -174,6 +185,7 @@ ALIASES = {
     "c3": "gqa32x8_b16_d128_n8192",
     "c4": "mqa32_b32_d128_n16384",
     "c5": "gqa64x8_b4_d128_ragged64k-128k_64steps",
+    "spec4": "gqa64x8_b4_d128_ragged64k-128k_16steps_x4rows",
 }
 
 
@@ -186,11 +198,12 @@ class Inputs:
     shape: Shape
     lens: np.ndarray            # int32 [B], initial lengths
     q: np.ndarray               # float32 [B, h_q, d_k], query of the first decode
+                                # ([B, h_q, rows, d_k] when rows > 1)
     K: np.ndarray               # float32 [B, h_kv, n_max, d_k]
     V: np.ndarray               # float32 [B, h_kv, n_max, d_v]
-    k_new: np.ndarray           # float32 [steps, B, h_kv, d_k]
-    v_new: np.ndarray           # float32 [steps, B, h_kv, d_v]
-    q_step: np.ndarray          # float32 [steps, B, h_q, d_k]
+    k_new: np.ndarray           # float32 [steps, B, h_kv, d_k]   (rows > 1: [.., rows, d_k])
+    v_new: np.ndarray           # float32 [steps, B, h_kv, d_v]   (rows > 1: [.., rows, d_v])
+    q_step: np.ndarray          # float32 [steps, B, h_q, d_k]    (rows > 1: [.., rows, d_k])
 
 
 def draw_lengths(shape: Shape, seed: int = 0) -> np.ndarray:
@@ -206,25 +219,26 @@ def make(shape: Shape, seed: int = 0, pad: float = float("nan"),
     if lens is None:
         lens = draw_lengths(s, seed)
     lens = np.ascontiguousarray(lens, dtype=np.int32)
-    q = normal(seed, 1, (s.B, s.h_q, s.d_k), threads)
+    r = () if s.rows == 1 else (s.rows,)
+    q = normal(seed, 1, (s.B, s.h_q) + r + (s.d_k,), threads)
     K = cache(seed, 2, lens, s.h_kv, s.n_max, s.d_k, pad, threads)
     V = cache(seed, 3, lens, s.h_kv, s.n_max, s.d_v, pad, threads)
-    kn = np.empty((s.steps, s.B, s.h_kv, s.d_k), np.float32)
-    vn = np.empty((s.steps, s.B, s.h_kv, s.d_v), np.float32)
-    qs = np.empty((s.steps, s.B, s.h_q, s.d_k), np.float32)
+    kn = np.empty((s.steps, s.B, s.h_kv) + r + (s.d_k,), np.float32)
+    vn = np.empty((s.steps, s.B, s.h_kv) + r + (s.d_v,), np.float32)
+    qs = np.empty((s.steps, s.B, s.h_q) + r + (s.d_k,), np.float32)
     for t in range(s.steps):
-        kn[t] = normal(seed, 4 + 3 * t, (s.B, s.h_kv, s.d_k), threads)
-        vn[t] = normal(seed, 5 + 3 * t, (s.B, s.h_kv, s.d_v), threads)
-        qs[t] = normal(seed, 6 + 3 * t, (s.B, s.h_q, s.d_k), threads)
+        kn[t] = normal(seed, 4 + 3 * t, kn.shape[1:], threads)
+        vn[t] = normal(seed, 5 + 3 * t, vn.shape[1:], threads)
+        qs[t] = normal(seed, 6 + 3 * t, qs.shape[1:], threads)
     return Inputs(s, lens, q, K, V, kn, vn, qs)
 
 
 def custom(name: str = "custom", *, B: int, h_q: int, h_kv: int, d_k: int,
            d_v: int, n_max: int, len_lo: int | None = None,
            len_hi: int | None = None, steps: int = 0,
-           scale: float = 0.0) -> Shape:
+           scale: float = 0.0, rows: int = 1) -> Shape:
     """A workload of arbitrary shape (tests: ragged tails, edge cases)."""
     lo = n_max if len_lo is None else len_lo
     hi = lo if len_hi is None else len_hi
     return Shape(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v, n_max=n_max,
-                 len_lo=lo, len_hi=hi, steps=steps, scale=scale)
+                 len_lo=lo, len_hi=hi, steps=steps, scale=scale, rows=rows)

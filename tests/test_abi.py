@@ -140,6 +140,41 @@ def test_step_validation():
     assert S(*a) == 3
 
 
+def test_multi_row_validation():
+    D = lib.da_decode_multi
+    base = [FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, 0, FAKE, 1 << 20, None]
+    for pos in (0, 1, 2, 3, 5):
+        a = list(base); a[pos] = None
+        assert D(*a) == 1, pos
+    for T in (0, -1, 4097):
+        a = list(base); a[12] = T
+        assert D(*a) == 2, T
+    a = list(base); a[15] = 16
+    assert D(*a) == 6
+    a = list(base); a[5] = FAKE + 4
+    assert D(*a) == 4
+    S = lib.da_decode_multi_step
+    sb = [FAKE] * 6 + [0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, 0, FAKE, 1 << 20, None]
+    for pos in (3, 4, 5, 7):
+        a = list(sb); a[pos] = None
+        assert S(*a) == 1, pos
+    a = list(sb); a[14] = 0
+    assert S(*a) == 2
+    R = lib.da_kv_append_rows
+    rb = [FAKE] * 5 + [1, 1, 8, 64, 64, 3, None]
+    assert R(*rb[:4], None, *rb[5:]) == 1
+    for T in (0, 4097):
+        a = list(rb); a[10] = T
+        assert R(*a) == 2, T
+    a = list(rb); a[8] = 62
+    assert R(*a) == 3
+    a = list(rb); a[2] = FAKE + 4
+    assert R(*a) == 4
+    # the workspace of a T-row decode is that of h_q*T query heads
+    assert binding.workspace_bytes(2, 8 * 4, 2, 1000, 128, 128) > binding.workspace_bytes(
+        2, 8, 2, 1000, 128, 128)
+
+
 @pytest.mark.parametrize("args,status", [
     ((None, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64), 1),
     ((FAKE, FAKE, FAKE, FAKE, None, 1, 1, 8, 64, 64), 1),

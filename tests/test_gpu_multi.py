@@ -1,0 +1,183 @@
+"""Parity of the multi-row (causal) decode, the fused multi-row step and the
+T-row append on the GPU (through the C ABI) with the CPU oracle.
+
+Decode: max-abs-err <= 1e-5 against the fp64 oracle on seeded N(0,1) inputs,
+cache rows at or beyond len[b] poisoned with NaN; rows with no visible key
+must be exactly zero.  Appends: bit-exact.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_19456_amd import binding, workloads
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def dev(a, device):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def rand(seed, shape):
+    from paper_2607_19456_amd.workloads import normal
+    return normal(seed, 77, shape)
+
+
+def poisoned_multi_workspace(dq, dK, dV, chunk_rows=0):
+    ws = binding.alloc_multi_workspace(dq, dK, dV, chunk_rows)
+    ws.fill_(0xFF)
+    B, h_q, T, d_k = dq.shape
+    _, h_kv, n_max, _ = dK.shape
+    nc = binding.workspace_counter_bytes(B, h_q * T, h_kv, n_max, d_k, dV.shape[3])
+    ws[:nc].zero_()
+    return ws, nc
+
+
+def check(got, ref, what):
+    assert got.shape == ref.shape
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    say(f"  {what}: max-abs-err {err:.3e}")
+    assert err <= TOL, f"{what}: max-abs-err {err:.3e} > {TOL}"
+
+
+MULTI = [
+    # name, B, h_q, h_kv, d_k, d_v, n_max, T, lens
+    ("gqa8_T4", 2, 16, 2, 128, 128, 900, 4, [900, 37]),
+    ("mha_d64_T2", 2, 4, 4, 64, 64, 300, 2, [300, 1]),
+    ("mqa32_T3_headgroups", 2, 32, 1, 128, 128, 513, 3, [513, 2]),
+    ("dk64_dv128_T8", 2, 8, 2, 64, 128, 400, 8, [400, 5]),
+    ("T16_two_groups", 1, 4, 1, 128, 128, 1000, 16, [1000]),
+    ("dk128_dv64_T5_odd", 3, 6, 3, 128, 64, 97, 5, [97, 4, 60]),
+    ("empty_and_short", 2, 8, 4, 128, 128, 70, 4, [0, 3]),
+]
+
+
+@pytest.mark.parametrize("case", MULTI, ids=[c[0] for c in MULTI])
+@pytest.mark.parametrize("chunk_rows", [0, 384])
+def test_decode_multi(cuda_device, case, chunk_rows):
+    name, B, h_q, h_kv, d_k, d_v, n_max, T, lens = case
+    shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v, n_max=n_max)
+    seed = zlib.crc32(name.encode()) % 1000
+    inp = workloads.make(shape, seed=seed, lens=np.array(lens, np.int32))
+    q = rand(seed, (B, h_q, T, d_k))
+    say(f"decode_multi {name} T={T} chunk_rows={chunk_rows} lens={lens}")
+    dq, dK, dV = dev(q, cuda_device), dev(inp.K, cuda_device), dev(inp.V, cuda_device)
+    dl = dev(inp.lens, cuda_device)
+    ws, nc = poisoned_multi_workspace(dq, dK, dV, chunk_rows)
+    out = binding.decode_multi(dq, dK, dV, dl, float(shape.scale32()), workspace=ws,
+                               chunk_rows=chunk_rows)
+    torch.cuda.synchronize()
+    assert not ws[:nc].any(), "counters not reset by the merge"
+    got = out.cpu().numpy().astype(np.float64)
+    ref = oracle.decode_multi(q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, name)
+    for b, n in enumerate(lens):
+        for r in range(T):
+            if n - T + r < 0:
+                assert not got[b, :, r].any(), (b, r)
+
+
+STEPS = [
+    # name, B, h_q, h_kv, d_k, d_v, n_max, T, lens
+    ("gqa8_T4", 3, 16, 2, 128, 128, 700, 4, [0, 333, 698]),     # empty, middle, clipped
+    ("mha_d64_T2_full", 2, 4, 4, 64, 64, 300, 2, [299, 300]),   # one row fits / none
+    ("mqa_T3_dkdv", 2, 32, 1, 64, 128, 200, 3, [5, 190]),
+    ("neg_len_T6", 2, 8, 4, 128, 128, 100, 6, [-3, 40]),
+]
+
+
+@pytest.mark.parametrize("case", STEPS, ids=[c[0] for c in STEPS])
+def test_decode_multi_step_equals_sequential_steps(cuda_device, case):
+    name, B, h_q, h_kv, d_k, d_v, n_max, T, lens = case
+    shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v, n_max=n_max)
+    seed = zlib.crc32(name.encode()) % 1000
+    inp = workloads.make(shape, seed=seed, lens=np.array(lens, np.int32))
+    dK, dV, dl = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    hK, hV, hl = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    ws = None
+    for step in range(2):
+        q = rand(seed + 10 * step, (B, h_q, T, d_k))
+        kn = rand(seed + 10 * step + 1, (B, h_kv, T, d_k))
+        vn = rand(seed + 10 * step + 2, (B, h_kv, T, d_v))
+        dq = dev(q, cuda_device)
+        if ws is None:
+            ws, nc = poisoned_multi_workspace(dq, dK, dV)
+        say(f"multi step {name} step {step} len={hl.tolist()}")
+        out = binding.decode_multi_step(dq, dK, dV, dev(kn, cuda_device), dev(vn, cuda_device),
+                                        dl, float(shape.scale32()), workspace=ws)
+        torch.cuda.synchronize()
+        # the definition: T single steps (append one row, decode its query)
+        ref = np.zeros((B, h_q, T, d_v))
+        for r in range(T):
+            oracle.append(hK, hV, np.ascontiguousarray(kn[:, :, r]),
+                          np.ascontiguousarray(vn[:, :, r]), hl)
+            ref[:, :, r] = oracle.decode(np.ascontiguousarray(q[:, :, r]), hK, hV, hl,
+                                         shape.scale32())
+        assert dl.cpu().numpy().tolist() == hl.tolist()
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))
+        assert np.array_equal(dV.cpu().numpy().view(np.uint32), hV.view(np.uint32))
+        assert not ws[:nc].any()
+        check(out.cpu().numpy().astype(np.float64), ref, f"{name} step {step}")
+
+
+@pytest.mark.parametrize("T", [1, 3, 8])
+def test_append_rows_bit_exact(cuda_device, T):
+    B, h_kv, n_max, d_k, d_v = 4, 3, 12, 8, 12
+    rng = np.random.default_rng(T)
+    K = rng.standard_normal((B, h_kv, n_max, d_k)).astype(np.float32)
+    V = rng.standard_normal((B, h_kv, n_max, d_v)).astype(np.float32)
+    lens = np.array([0, 5, 11, -2], np.int32)
+    dK, dV, dl = dev(K, cuda_device), dev(V, cuda_device), dev(lens, cuda_device)
+    for step in range(3):
+        kn = rng.standard_normal((B, h_kv, T, d_k)).astype(np.float32)
+        vn = rng.standard_normal((B, h_kv, T, d_v)).astype(np.float32)
+        kn.view(np.uint32)[0, 0, 0, :3] = [0x7FC01234, 0x80000000, 0x00000001]
+        say(f"append_rows T={T} step {step}")
+        binding.kv_append_rows(dK, dV, dev(kn, cuda_device), dev(vn, cuda_device), dl)
+        oracle.append_rows(K, V, kn, vn, lens)
+        torch.cuda.synchronize()
+        assert np.array_equal(dl.cpu().numpy(), lens)
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), K.view(np.uint32))
+        assert np.array_equal(dV.cpu().numpy().view(np.uint32), V.view(np.uint32))
+
+
+def test_multi_row_long_context_sampled(cuda_device):
+    """The 4-row speculative workload's first steps through the fused path,
+    checked on sampled heads (the host mirror replays the appends)."""
+    shape = workloads.get("spec4")
+    say("multi-row long context: generating inputs")
+    inp = workloads.make(shape, seed=4)
+    dK, dV, dl = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    hK, hV, hl = inp.K, inp.V, inp.lens.copy()
+    ws = binding.alloc_multi_workspace(dev(inp.q_step[0], cuda_device), dK, dV)
+    T = shape.rows
+    rng = np.random.default_rng(5)
+    for t in range(3):
+        out = binding.decode_multi_step(dev(inp.q_step[t], cuda_device), dK, dV,
+                                        dev(inp.k_new[t], cuda_device),
+                                        dev(inp.v_new[t], cuda_device), dl,
+                                        float(shape.scale32()), workspace=ws)
+        len0 = hl.copy()
+        oracle.append_rows(hK, hV, inp.k_new[t], inp.v_new[t], hl)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().astype(np.float64)
+        heads = np.zeros((shape.B, shape.h_q), bool)
+        for b in range(shape.B):
+            heads[b, rng.choice(shape.h_q, 3, replace=False)] = True
+            heads[b, 0] = heads[b, -1] = True
+        for r in range(T):
+            lens_r = np.minimum(len0 + r + 1, shape.n_max).astype(np.int32)
+            ref = oracle.decode(np.ascontiguousarray(inp.q_step[t][:, :, r]), hK, hV, lens_r,
+                                shape.scale32(), heads=heads)
+            check(got[:, :, r][heads], ref[heads], f"spec4 step {t} row {r}")
+        assert dl.cpu().numpy().tolist() == hl.tolist()
