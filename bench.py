@@ -120,6 +120,84 @@ def cpu_baseline(inp, budget_s: float, step_bytes):
     }
 
 
+def conventional_leg(s, inp, dev, our_us_per_step, steps_cap=8, outputs=None):
+    """The conventional PyTorch path on the same GPU and inputs: a cache that
+    grows by ``torch.cat`` at every step (an O(t) copy instead of an
+    O(d_k+d_v) append) and GQA by ``repeat_interleave`` of the KV heads (h_q
+    copies of each KV row materialised and read instead of h_kv), then
+    scores, softmax and the weighted sum as separate fp32 tensor operations.
+    Sequences are handled one by one (their caches have different lengths).
+    Returns timing and a byte model; the inputs are this workload's own."""
+    import numpy as np
+    import torch
+
+    G = s.h_q // s.h_kv
+    scale = float(s.scale32())
+    # multi-step workloads: step 0 warms up, steps 1.. are timed (at most
+    # steps_cap of them); a single decode is repeated on the same cache
+    total = min(s.steps, steps_cap + 1) if s.steps else 1
+    warm = 1 if total > 1 or not s.steps else 0
+    timed = list(range(warm, total)) if s.steps else [0]
+    Kb = [torch.from_numpy(np.ascontiguousarray(inp.K[b, :, :int(inp.lens[b])])).to(dev)
+          for b in range(s.B)]
+    Vb = [torch.from_numpy(np.ascontiguousarray(inp.V[b, :, :int(inp.lens[b])])).to(dev)
+          for b in range(s.B)]
+    if s.steps:
+        kn = torch.from_numpy(inp.k_new[:total]).to(dev)
+        vn = torch.from_numpy(inp.v_new[:total]).to(dev)
+        qs = torch.from_numpy(inp.q_step[:total]).to(dev)
+    else:
+        qs = torch.from_numpy(inp.q[None]).to(dev)
+    out = torch.empty((s.B, s.h_q, s.d_v), dtype=torch.float32, device=dev)
+
+    def one_step(t):
+        for b in range(s.B):
+            if s.steps:
+                Kb[b] = torch.cat([Kb[b], kn[t, b][:, None, :]], dim=1)
+                Vb[b] = torch.cat([Vb[b], vn[t, b][:, None, :]], dim=1)
+            Kx = Kb[b].repeat_interleave(G, dim=0) if G > 1 else Kb[b]   # [h_q, n, d_k]
+            Vx = Vb[b].repeat_interleave(G, dim=0) if G > 1 else Vb[b]
+            sc = torch.matmul(Kx, qs[t, b][:, :, None])[..., 0] * scale  # [h_q, n]
+            a = torch.softmax(sc, dim=-1)
+            out[b] = torch.matmul(a[:, None, :].contiguous(), Vx)[:, 0]
+
+    if warm:
+        one_step(0)                               # warm-up (allocator, kernels)
+        torch.cuda.synchronize()
+        if outputs is not None:                   # for the parity test
+            outputs.append(out.double().cpu().numpy())
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for t in timed:
+        one_step(t)
+        if outputs is not None:
+            torch.cuda.synchronize()
+            outputs.append(out.double().cpu().numpy())
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) * 1e3 / len(timed)
+    lens = [int(Kb[b].shape[1]) for b in range(s.B)]
+    F32 = 4
+    d = s.d_k + s.d_v
+    kv = sum(s.h_kv * n * d * F32 for n in lens)
+    cat = 2 * kv if s.steps else 0                 # read the old cache, write the new one
+    rep = (kv + G * kv) if G > 1 else 0           # read h_kv rows, write h_q copies
+    attn = G * kv + s.B * s.h_q * d * F32         # read h_q rows per head, q, out
+    return {
+        "us_per_step": round(us, 2),
+        "steps_timed": len(timed),
+        "this_path_us_per_step": round(our_us_per_step, 2),
+        "speedup_of_this_path": round(us / our_us_per_step, 2),
+        "append": "torch.cat (the cache grows by a full copy each step)" if s.steps else None,
+        "gqa": f"repeat_interleave x{G}" if G > 1 else None,
+        "hbm_bytes_model_per_step": int(cat + rep + attn),
+        "this_path_hbm_bytes_per_step": int(kv + s.B * s.h_q * d * F32 +
+                                            (s.B * s.h_kv * d * F32 if s.steps else 0)),
+        "final_len": lens,
+    }
+
+
 def _cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -140,6 +218,9 @@ def main() -> int:
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--conventional", action="store_true",
+                    help="also time the conventional PyTorch path (torch.cat cache, "
+                         "repeat_interleave GQA) on the same inputs")
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed steps in one HIP graph and replay it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -355,6 +436,14 @@ def main() -> int:
 
     del dK, dV
     torch.cuda.empty_cache()
+    if args.conventional:
+        if s.rows > 1:
+            result["conventional"] = None
+        else:
+            log("conventional PyTorch path on the same inputs")
+            result["conventional"] = conventional_leg(s, inp, dev, ms_per_step * 1e3)
+            log(f"conventional: {result['conventional']['us_per_step']} us/step")
+            torch.cuda.empty_cache()
     if args.cpu_seconds > 0:
         log("cpu_baseline: timing the oracle on this host")
         # the oracle replays the workload from its initial state
