@@ -53,18 +53,25 @@ constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgr
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
 // Register tiles per wave in the load ring, and waves per SIMD, of the
-// partial kernel: a three-tile ring at one wave per SIMD keeps two tiles'
-// loads in flight during each tile's products.  (Measured alternatives: two
-// tiles at two waves per SIMD is slower both for groups of <= 16 heads and
-// for groups of 17..32, whose two column blocks double the matrix work.)
+// partial kernel.  One column block (<= 16 query rows per KV head): a
+// three-tile ring at one wave per SIMD keeps two tiles' loads in flight
+// during each tile's products (two tiles at two waves per SIMD measured the
+// same on long contexts and 2-3 % slower on the shorter ones).  Two column
+// blocks double the matrix work per tile: there a two-tile ring at two waves
+// per SIMD, whose registers fit without parking the accumulators in AGPRs and
+// whose second wave overlaps one wave's softmax with the other's products,
+// is 5 % (MQA) to 10 % (four query rows per head) faster.
 template <int NB>
-constexpr int kRing = 3;
+constexpr int kRing = NB == 2 ? 2 : 3;
 template <int NB>
-constexpr int kWavesPerSimd = 1;
+constexpr int kWavesPerSimd = NB == 2 ? 2 : 1;
 // A chunk is the rows a workgroup takes at a time: a multiple of six 16-row
-// tiles per wave (whole turns of the three-tile ring).
+// tiles per wave (whole turns of either ring).  The default is 768 rows for
+// one column block and 384 for two, whose twice as many resident workgroups
+// need more chunks to share the tail (measured).
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 constexpr int kDefaultChunkRows = 768;
+constexpr int kDefaultChunkRows2 = 384;
 // Visit slots per slab, in units of the even share of waves per slab.
 constexpr int kVisitSlack = 4;
 constexpr int64_t kMaxSlabs = 1 << 20;
@@ -374,14 +381,14 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //
 // A slab is the cache rows of one (b, KV head, head group); it is cut into
 // chunks of C rows handed out by a per-slab counter.  A fixed set of
-// workgroups (one per CU) stays resident; each one opens a "visit" on a slab
-// with chunks left (taking, in one atomic step, its first two chunks and a
-// visit slot j < J, so every visit has rows and the slots in use are exactly
-// 0 .. visits-1), takes chunks from that slab's counter until none are left
-// -- its four waves interleave the chunk's 16-row tiles, so the workgroup
-// streams one contiguous run of K and of V -- and folds all of them into one
-// running (max, sum, weighted sum) state, since the online softmax does not
-// care which rows it has seen.  It then writes one partial per query head to
+// workgroups (one per CU and wave slot) stays resident; each one opens a
+// "visit" on a slab with chunks left (taking, in one atomic step, its first
+// two chunks and a visit slot j < J, so every visit has rows and the slots in
+// use are exactly 0 .. visits-1), takes chunks from that slab's counter until
+// none are left -- its four waves interleave the chunk's 16-row tiles, so the
+// workgroup streams one contiguous run of K and of V -- and folds all of them
+// into one running (max, sum, weighted sum) state, since the online softmax
+// does not care which rows it has seen.  It then writes one partial per query head to
 // slot j, counts the visit in each head's visit count and looks for the next
 // slab.  No CU idles while rows remain and faster CUs simply take more chunks.
 // Nothing here waits on another workgroup or needs a device-wide fence: the
@@ -817,9 +824,9 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
                     Plan* plan) {
   da_status st = check_shapes(B, h_q, h_kv, n_max, d_k, d_v);
   if (st != DA_OK) return st;
-  if (chunk_rows == 0) chunk_rows = kDefaultChunkRows;
-  if (chunk_rows < kChunkQuantum || chunk_rows % kChunkQuantum != 0) return DA_ERR_SHAPE;
   const int G = h_q / h_kv;
+  if (chunk_rows == 0) chunk_rows = G > kHeadsPerBlock ? kDefaultChunkRows2 : kDefaultChunkRows;
+  if (chunk_rows < kChunkQuantum || chunk_rows % kChunkQuantum != 0) return DA_ERR_SHAPE;
   plan->chunk_rows = chunk_rows;
   plan->head_groups = (int)ceil_div(G, kHeadsPerGroup);
   plan->blocks = G > kHeadsPerBlock ? 2 : 1;
