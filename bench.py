@@ -50,9 +50,13 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_build_hash() -> str:
+    """sha256 of the kernel source and the compiler flags it is built with
+    (either changes the code the counters were taken on)."""
+    from paper_2607_19456_amd import build
     with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+        src = f.read()
+    return hashlib.sha256(src + "\n".join(build.FLAGS).encode()).hexdigest()
 
 
 def counter_traffic(workload: str):
@@ -63,7 +67,7 @@ def counter_traffic(workload: str):
             c = json.load(f)
     except (OSError, ValueError):
         return None
-    if c.get("kernel_source_sha256") != kernel_source_hash() or c.get("workload") != workload:
+    if c.get("kernel_build_sha256") != kernel_build_hash() or c.get("workload") != workload:
         return None
     return c.get("hbm_bytes_per_launch")
 

@@ -27,6 +27,10 @@ FLAGS = [
     # rewrite reads the result at once, which stalls the load pipeline
     # behind the work counter of the decode kernel.
     "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
+    # Matrix-core results in VGPRs: the decode's accumulators then stay in
+    # the registers its softmax rescale works on, instead of being copied
+    # between AGPRs and VGPRs around every tile.
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{INCLUDE}",
 ]
 
