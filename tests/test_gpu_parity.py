@@ -210,6 +210,34 @@ def test_validation_errors_raise(cuda_device):
         binding.decode_attn(dq, dK, dV, dl, float("nan"))
 
 
+def test_thousands_of_slabs_ragged(cuda_device):
+    """2400 slabs (many more than resident workgroups, and than the 64 slabs
+    one search step looks at), ragged lengths from 0 to 300."""
+    B, h_q, h_kv, n_max = 300, 16, 8, 300
+    shape = workloads.custom("many_slabs", B=B, h_q=h_q, h_kv=h_kv, d_k=64, d_v=64,
+                             n_max=n_max)
+    lens = np.random.default_rng(3).integers(0, n_max + 1, size=B).astype(np.int32)
+    lens[:3] = [0, 1, n_max]
+    inp = workloads.make(shape, seed=13, lens=lens)
+    say("thousands of slabs: decode")
+    got = run_decode(inp, cuda_device)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, "2400 slabs")
+
+
+def test_two_million_rows_one_slab(cuda_device):
+    """One sequence of 2^21 + 5 rows (a slab of 512 MiB per tensor at d=64):
+    row offsets beyond 2^31 bytes."""
+    n = (1 << 21) + 5
+    shape = workloads.custom("huge", B=1, h_q=4, h_kv=1, d_k=64, d_v=64, n_max=n)
+    say("two million rows: generating inputs")
+    inp = workloads.make(shape, seed=14)
+    say("two million rows: decode")
+    got = run_decode(inp, cuda_device)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, "2^21+5 rows")
+
+
 # --- fused append + decode step ------------------------------------------------
 
 STEP_CASES = [
