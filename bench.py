@@ -274,10 +274,13 @@ def main() -> int:
     else:
         dq = torch.from_numpy(inp.q[None]).to(dev)
     multi = s.rows > 1
+    # A single decode whose slabs are each one chunk runs in the direct form
+    # (one launch writes the output): time da_decode_attn as a whole then.
     out = torch.empty((s.B, s.h_q) + ((s.rows,) if multi else ()) + (s.d_v,),
                       dtype=torch.float32, device=dev)
     chunk = args.chunk_rows or binding.chunk_rows(s.B, s.h_q * s.rows, s.h_kv, s.n_max,
                                                   s.d_k, s.d_v)
+    direct = not s.steps and not multi and chunk >= s.n_max
     if multi:
         ws = binding.alloc_multi_workspace(dq[0], dK, dV, chunk)
     else:
@@ -301,6 +304,12 @@ def main() -> int:
             # inside the events
             binding.decode_multi_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=out,
                                       workspace=ws, chunk_rows=chunk, stream=st)
+            if ev_b is not None:
+                ev_b.record(st)
+            return
+        if direct:
+            binding.decode_attn(dq[t], dK, dV, dl, scale, out=out, workspace=ws,
+                                chunk_rows=chunk, stream=st)
             if ev_b is not None:
                 ev_b.record(st)
             return
@@ -378,8 +387,8 @@ def main() -> int:
     alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
     # The partial kernel of a step also writes the appended rows (Prop. 2).
     append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v, s.rows) if s.steps else 0
-    if multi:   # the events hold the whole step (partial + merge)
-        launch_bytes = [step_bytes(l) for l in step_lens]
+    if multi or direct:   # the events hold the whole step
+        launch_bytes = [step_bytes(l, bool(s.steps)) for l in step_lens]
     else:
         launch_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
                         for l in step_lens]
@@ -411,6 +420,7 @@ def main() -> int:
             "chunk_rows": chunk,
             "step": ("da_decode_multi_step (T-row append fused, causal T-row decode)"
                      if multi else
+                     "da_decode_attn (direct form: one launch, no merge)" if direct else
                      "decode_partial with fused kv_append + decode_merge" if s.steps
                      else "decode_partial + decode_merge"),
             "graph": bool(args.graph),
@@ -422,15 +432,17 @@ def main() -> int:
         "roofline": {
             "bound": "hbm",
             "kernel": ("decode_partial_kernel + decode_merge_kernel (the whole step)"
-                       if multi else "decode_partial_kernel"),
+                       if multi else
+                       "decode_partial_kernel (direct form, the whole decode)" if direct
+                       else "decode_partial_kernel"),
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": None if multi else counter_traffic(s.name),
             "avg_launch_us": round(launch_avg_ms * 1e3, 2),
-            "timing": ("graph replay / steps (partial + merge)" if args.graph
-                       else "HIP events around each step (partial + merge)" if multi
+            "timing": ("graph replay / steps" if args.graph
+                       else "HIP events around each step" if multi or direct
                        else "HIP events around each partial launch"),
             "algorithmic_bytes_per_launch": int(sum(launch_bytes) / len(launch_bytes)),
         },

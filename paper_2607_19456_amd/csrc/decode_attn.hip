@@ -407,7 +407,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
     int B, int h_q, int h_kv, int n_max, int T, int C, int head_groups, int J,
     unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
-    float* __restrict__ ws_acc) {
+    float* __restrict__ ws_acc, float* __restrict__ out_direct) {
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
@@ -453,6 +453,10 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     }
   }
   int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
+  // Direct form (out_direct set; every slab is a single chunk): workgroup s
+  // owns slab s, takes its one chunk without searching and writes the output
+  // rows itself -- no merge, and no other workgroup touches its counter line.
+  bool first = true;
 
   while (true) {
     // ---- wave 0 opens a visit: a slab with chunks and slots left.  Lane 0
@@ -461,7 +465,13 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     // chunk and there are never more than J of them.
     if (wave == 0) {
       int s = -1, j = -1, c = -1, cn = -1;
-      int budget = S;
+      int budget = out_direct ? 0 : S;
+      if (out_direct && first) {
+        s = blockIdx.x;
+        j = 0;
+        c = 0;
+        cn = 1;
+      }
       while (budget > 0) {
         int seen;
         const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, T, C, J,
@@ -501,6 +511,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     int c = sh_ctl[2];
     int cn = sh_ctl[3];
     if (s < 0) break;                                   // every slab is exhausted
+    first = false;
 
     const int b = s / per_b;
     const int rem = s - b * per_b;
@@ -510,6 +521,14 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     const int n = decode_rows(len_b, n_max, app, T);
     const int nch = (n + C - 1) / C;
     const int last_row = n - 1;
+    if (out_direct && nch == 0) {
+      // An empty cache: the slab's output rows are zero.
+      const int hc = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
+      float* o = out_direct + ((int64_t)b * h_q + g * G + hgrp * (NB * kHeadsPerBlock)) * DV;
+      for (int e = tid; e < hc * (DV / 4); e += kThreads)
+        reinterpret_cast<f4*>(o)[e] = f4{0.f, 0.f, 0.f, 0.f};
+      break;
+    }
     const int h_first = g * G + hgrp * (NB * kHeadsPerBlock);
     const int h_count = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
     const int64_t slab = (int64_t)b * h_kv + g;
@@ -622,7 +641,9 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
             process_tile<DK, DV, NB, CAUSAL>(t1, r1, lim, k, lane, sh_q, m_run, l_run, acc);
           t += 2;
         }
-      } while (t < tpw);
+        // A wave whose remaining tiles all lie past the slab's end (only in the
+        // slab's last chunk) leaves early instead of idling through them.
+      } while (t < tpw && row_of(t, c, cn) <= last_row);
       if (tid == 0) sh_next[it & 1] = after;
       __syncthreads();
       if (cn >= nch) break;
@@ -681,21 +702,37 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
         if (hl < h_count) {
           const int64_t head = (int64_t)b * h_q + h_first + hl;
           const int64_t slot = head * J + j;
-          if (k == 0) {
-            ws_ml[slot] = make_float2(M, L);
-            atomicAdd(nvis + head, 1u);
+          float* dst;
+          float inv = 1.f;
+          if (out_direct) {
+            // The only visit of the slab: normalise and write the output row
+            // (a causal row that saw no key, L = 0, gives zeros).
+            dst = out_direct + head * DV;
+            inv = L > 0.f ? 1.f / L : 0.f;
+          } else {
+            dst = ws_acc + slot * DV;
+            if (k == 0) {
+              ws_ml[slot] = make_float2(M, L);
+              atomicAdd(nvis + head, 1u);
+            }
           }
-          float* dst = ws_acc + slot * DV;
 #pragma unroll
           for (int cc = 0; cc < DV / 64; ++cc)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const f4 o = f4{acc[nb][cc][0][r], acc[nb][cc][1][r], acc[nb][cc][2][r],
                               acc[nb][cc][3][r]};
-              *reinterpret_cast<f4*>(dst + 64 * cc + 16 * k + 4 * r) = o;
+              *reinterpret_cast<f4*>(dst + 64 * cc + 16 * k + 4 * r) = o * inv;
             }
         }
       }
+    }
+    if (out_direct) {
+      // Thread 0 issued this slab's only counter requests; clear the line
+      // for the next call (program order keeps the store after them).
+      if (tid == 0)
+        *reinterpret_cast<unsigned long long*>(cnt + (size_t)s * kCounterStride) = 0ull;
+      break;
     }
     // Wave 0 runs the next search; the barrier at its end keeps the other
     // waves from touching sh_q / sh_ctl before wave 0 is done here.
@@ -803,6 +840,7 @@ struct Plan {
   int grid;           // resident workgroups of the partial kernel
   int J;              // visit slots per (b, query head)
   int merge_heads;    // query heads per slab the merge covers
+  bool single_chunk;  // every slab fits in one chunk (direct form possible)
   size_t line_bytes, counter_bytes, ml_bytes, bytes;
 };
 
@@ -825,7 +863,12 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   da_status st = check_shapes(B, h_q, h_kv, n_max, d_k, d_v);
   if (st != DA_OK) return st;
   const int G = h_q / h_kv;
-  if (chunk_rows == 0) chunk_rows = G > kHeadsPerBlock ? kDefaultChunkRows2 : kDefaultChunkRows;
+  if (chunk_rows == 0) {
+    // The default, or the whole cache rounded up to the quantum if shorter.
+    chunk_rows = G > kHeadsPerBlock ? kDefaultChunkRows2 : kDefaultChunkRows;
+    chunk_rows = (int)std::min<int64_t>(chunk_rows,
+                                        ceil_div(n_max, kChunkQuantum) * kChunkQuantum);
+  }
   if (chunk_rows < kChunkQuantum || chunk_rows % kChunkQuantum != 0) return DA_ERR_SHAPE;
   plan->chunk_rows = chunk_rows;
   plan->head_groups = (int)ceil_div(G, kHeadsPerGroup);
@@ -833,6 +876,7 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   plan->slabs = B * h_kv * plan->head_groups;
   plan->merge_heads = std::min(G, plan->blocks * kHeadsPerBlock);
   const int64_t chunks_per_slab = ceil_div(n_max, chunk_rows);
+  plan->single_chunk = chunks_per_slab == 1;
   // One resident workgroup per CU and wave slot, fewer if there are fewer
   // chunks than that.
   const int64_t resident = (int64_t)kComputeUnits * (plan->blocks == 1 ? kWavesPerSimd<1>
@@ -883,14 +927,17 @@ struct PartialArgs {
   float qscale;
   int B, h_q, h_kv, n_max;   // h_q counts query rows: heads x T
   int T;                     // query rows per head (1: single-query decode)
+  float* out_direct;         // set: single-chunk slabs, output written directly
 };
 
 template <int DK, int DV, int NB, bool CAUSAL>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL>), dim3(pl.grid), dim3(kThreads),
+  // The direct form runs one workgroup per slab; otherwise the resident grid.
+  const unsigned grid = a.out_direct ? (unsigned)pl.slabs : (unsigned)pl.grid;
+  hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL>), dim3(grid), dim3(kThreads),
                      0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
                      a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.nvis,
-                     w.ml, w.acc);
+                     w.ml, w.acc, a.out_direct);
 }
 
 template <int DK, int DV>
@@ -923,7 +970,7 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
                        const float* v_new, const int32_t* len, float scale, int B, int h_q,
                        int h_kv, int n_max, int d_k, int d_v, int T, int chunk_rows,
                        void* workspace, size_t workspace_bytes, void* stream, const float* out,
-                       bool need_out, Plan* out_plan) {
+                       bool need_out, Plan* out_plan, bool allow_direct = false) {
   if (!q || !K || !V || !len || (need_out && !out)) return DA_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return DA_ERR_NULL;
   const int rows = query_rows(h_q, T);
@@ -941,8 +988,11 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
 
   const WsView w = view(pl, workspace);
   // K and V are written only when a fused append is asked for (k_new set).
+  // Direct form: only for a whole decode without a fused append (len is not
+  // advanced) whose slabs are single chunks.
+  float* direct = allow_direct && !k_new && pl.single_chunk ? const_cast<float*>(out) : nullptr;
   const PartialArgs a{q, const_cast<float*>(K), const_cast<float*>(V), k_new, v_new, len,
-                      scale * kLog2e, B, rows, h_kv, n_max, T};
+                      scale * kLog2e, B, rows, h_kv, n_max, T, direct};
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, a, w, s);
@@ -1057,8 +1107,9 @@ da_status da_decode_multi(const float* q, const float* K, const float* V, const 
   Plan pl;
   da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
                               d_v, T, chunk_rows, workspace, workspace_bytes, stream, out, true,
-                              &pl);
+                              &pl, true);
   if (st != DA_OK) return st;
+  if (pl.single_chunk) return DA_OK;                  // the direct form wrote out
   return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
 }

@@ -64,7 +64,8 @@ def test_chunk_rows_and_workspace_sizes():
                  (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
                  (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]:
         c = binding.chunk_rows(*args)
-        assert c == (384 if args[1] // args[2] > 16 else 768)
+        default = 384 if args[1] // args[2] > 16 else 768
+        assert c == min(default, -(-args[3] // 384) * 384)
         counters, total = _expected_workspace(*args, c)
         assert binding.workspace_counter_bytes(*args) == counters
         assert binding.workspace_bytes(*args) == total
