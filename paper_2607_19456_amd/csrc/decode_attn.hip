@@ -2,13 +2,18 @@
 // attention over a KV cache (MHA/GQA/MQA) and the per-step KV append.
 //
 // Kernels
-//   kv_append_kernel  eqs. (6)-(7): one bit-exact row copy per KV head, then
-//                     len[b] += 1 (Proposition 2's (d_k+d_v)*4 bytes).
+//   kv_append_kernel       eqs. (6)-(7): bit-exact row copies per KV head,
+//                          then len[b] += rows (Proposition 2's (d_k+d_v)*4
+//                          bytes per row); T rows at once for multi-row steps.
 //   decode_partial_kernel  eqs. (1)-(3) for all query heads of each GQA group
 //                          at once, as per-visit partial states: every KV slab
 //                          is read from HBM once and feeds all heads of its
 //                          group (the group caching of the GQA section).
 //                          Optionally fused with the append of the same step.
+//                          The CAUSAL instances serve T query rows per head
+//                          (a step that submits T positions); the direct form
+//                          (one workgroup per single-chunk slab) writes the
+//                          output itself.
 //   decode_merge_kernel    combines each head's partials into its output row
 //                          and resets the scheduling state.
 //
@@ -72,7 +77,8 @@ constexpr int kWavesPerSimd = NB == 2 ? 2 : 1;
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 constexpr int kDefaultChunkRows = 768;
 constexpr int kDefaultChunkRows2 = 384;
-// Visit slots per slab, in units of the even share of waves per slab.
+// Visit slots per slab, in units of the even share of resident workgroups per
+// slab.
 constexpr int kVisitSlack = 4;
 constexpr int64_t kMaxSlabs = 1 << 20;
 constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
@@ -231,7 +237,8 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
     for (int rho = 0; rho < 4; ++rho)
 #pragma unroll
       for (int c = 0; c < DV / 64; ++c)
-        T.v[rho][c] = load4_stream(reinterpret_cast<const float*>(vb + src.v_lane) + rho * DV + 64 * c);
+        T.v[rho][c] =
+            load4_stream(reinterpret_cast<const float*>(vb + src.v_lane) + rho * DV + 64 * c);
     return;
   }
   // The slab's last tile(s): rows past the end clamp to the last row, and
@@ -388,9 +395,9 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 // none are left -- its four waves interleave the chunk's 16-row tiles, so the
 // workgroup streams one contiguous run of K and of V -- and folds all of them
 // into one running (max, sum, weighted sum) state, since the online softmax
-// does not care which rows it has seen.  It then writes one partial per query head to
-// slot j, counts the visit in each head's visit count and looks for the next
-// slab.  No CU idles while rows remain and faster CUs simply take more chunks.
+// does not care which rows it has seen.  It then writes one partial per query
+// head to slot j, counts the visit in each head's visit count and looks for
+// the next slab.  No CU idles while rows remain and faster CUs simply take more chunks.
 // Nothing here waits on another workgroup or needs a device-wide fence: the
 // merge, a separate launch, sees every partial.
 //
@@ -603,7 +610,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
     };
     Tile<DK, DV, NB> t0, t1, t2;
     load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(0, c, cn), last_row, i, k);
-    if constexpr (kRing<NB> == 3) load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(1, c, cn), last_row, i, k);
+    if constexpr (kRing<NB> == 3)
+      load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(1, c, cn), last_row, i, k);
     for (int it = 0;; ++it) {
       // Thread 0 asks for the chunk after next even on the last chunk (the
       // counter simply runs past the end): a conditional request would merge
@@ -810,7 +818,8 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
         O += sh_o[p * kCols + ch] * w;
       }
     }
-    *reinterpret_cast<f4*>(out + row * DV + 4 * ch) = M != -INFINITY ? O / L : f4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f4*>(out + row * DV + 4 * ch) =
+        M != -INFINITY ? O / L : f4{0.f, 0.f, 0.f, 0.f};
   }
   if (tid == 0) {
     nvis[row] = 0u;
