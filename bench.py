@@ -80,9 +80,11 @@ def host_cores() -> int:
     return max(1, min(16, n))
 
 
-def cpu_baseline(inp, budget_s: float, step_bytes):
+def cpu_baseline(inp, budget_s: float, step_bytes, gpu_first=None):
     """Time the oracle (append + decode of every head, step after step) on
-    this host until about budget_s seconds of work are done."""
+    this host until about budget_s seconds of work are done.  With
+    ``gpu_first`` (the GPU's output of the first step, every head), also
+    return the max-abs-err between it and the oracle's first step."""
     import numpy as np
 
     import oracle
@@ -92,20 +94,23 @@ def cpu_baseline(inp, budget_s: float, step_bytes):
     hK, hV, hl = inp.K, inp.V, inp.lens.copy()
     done, elapsed, nbytes = 0, 0.0, 0
     steps = max(1, s.steps)
+    err = None
     while True:
         t = done % steps
         t0 = time.perf_counter()
         if s.rows > 1:
             oracle.append_rows(hK, hV, inp.k_new[t], inp.v_new[t], hl)
-            oracle.decode_multi(inp.q_step[t], hK, hV, hl, s.scale32(), threads=threads)
+            ref = oracle.decode_multi(inp.q_step[t], hK, hV, hl, s.scale32(), threads=threads)
         else:
             if s.steps:
                 oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
                 q = inp.q_step[t]
             else:
                 q = inp.q
-            oracle.decode(q, hK, hV, hl, s.scale32(), threads=threads)
+            ref = oracle.decode(q, hK, hV, hl, s.scale32(), threads=threads)
         elapsed += time.perf_counter() - t0
+        if done == 0 and gpu_first is not None:
+            err = float(np.max(np.abs(gpu_first - ref)))
         nbytes += step_bytes(hl, bool(s.steps))
         done += 1
         log(f"cpu_baseline: oracle step {done} ({elapsed:.1f} s)")
@@ -116,11 +121,12 @@ def cpu_baseline(inp, budget_s: float, step_bytes):
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"{done} full step(s) (append + decode of all {s.B * s.h_q * s.rows} "
-                   f"query rows) of the same workload, {elapsed:.2f} s, fp64 oracle, "
-                   f"{threads} OpenMP threads"),
+        "sample": (f"{done} full step(s) ({'append + ' if s.steps else ''}decode of all "
+                   f"{s.B * s.h_q * s.rows} query rows) of the same workload, {elapsed:.2f} s, "
+                   f"fp64 oracle, {threads} OpenMP threads"),
         "seconds_per_step": elapsed / done,
         "cpu_model": _cpu_model(),
+        "max_abs_err_first_step": err,
     }
 
 
@@ -450,6 +456,14 @@ def main() -> int:
     log(f"{ms_per_step * 1e3:.1f} us/step, {value:.0f} GB/s; partial "
         f"{launch_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
 
+    first_out = None
+    if args.cpu_seconds > 0:
+        # The first step once more from the initial lengths (it rewrites its
+        # appended rows with the same values), for the oracle check below.
+        dl.copy_(lens0)
+        step(0)
+        torch.cuda.synchronize()
+        first_out = out.double().cpu().numpy()
     del dK, dV
     torch.cuda.empty_cache()
     if args.conventional:
@@ -463,7 +477,9 @@ def main() -> int:
     if args.cpu_seconds > 0:
         log("cpu_baseline: timing the oracle on this host")
         # the oracle replays the workload from its initial state
-        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, step_bytes)
+        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, step_bytes, first_out)
+        result["max_abs_err_vs_oracle"] = result["cpu_baseline"]["max_abs_err_first_step"]
+        log(f"max-abs-err of the first step vs the oracle: {result['max_abs_err_vs_oracle']:.3e}")
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
