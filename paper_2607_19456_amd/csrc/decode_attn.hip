@@ -75,6 +75,7 @@ constexpr int kWavesPerSimd = NB == 2 ? 2 : 1;
 // one column block and 384 for two, whose twice as many resident workgroups
 // need more chunks to share the tail (measured).
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
+static_assert(6 % kRing<1> == 0 && 6 % kRing<2> == 0, "chunks are whole turns of the ring");
 constexpr int kDefaultChunkRows = 768;
 constexpr int kDefaultChunkRows2 = 384;
 // Visit slots per slab, in units of the even share of resident workgroups per
@@ -598,7 +599,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
 
     // The wave's tiles of chunk x: rows x*C + (4t + wave)*16, t < tpw.  The
     // register tiles form a ring: while one tile is on the matrix cores the
-    // loads of the next one or two are in flight, across chunk boundaries
+    // loads of the next R-1 are in flight, across chunk boundaries
     // too (tile x of the wave's sequence: x < tpw in this chunk, then the next
     // chunk's; past the visit's end the clamped last row, already cached, is
     // loaded so every path keeps the same loads in flight).  The chunk after
@@ -608,10 +609,11 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
                      : (cnn < nch ? cnn * C + (x - tpw) * (kWaves * kTileRows) + wave * kTileRows
                                   : last_row);
     };
-    Tile<DK, DV, NB> t0, t1, t2;
-    load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(0, c, cn), last_row, i, k);
-    if constexpr (kRing<NB> == 3)
-      load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(1, c, cn), last_row, i, k);
+    constexpr int R = kRing<NB>;
+    Tile<DK, DV, NB> ring[R];
+#pragma unroll
+    for (int p = 0; p < R - 1; ++p)
+      load_tile<DK, DV, NB, CAUSAL>(ring[p], src, row_of(p, c, cn), last_row, i, k);
     for (int it = 0;; ++it) {
       // Thread 0 asks for the chunk after next even on the last chunk (the
       // counter simply runs past the end): a conditional request would merge
@@ -622,33 +624,20 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
       // its first wait on a tile load the compiler knows the atomic issued
       // above (an older memory operation) has returned, so publishing its
       // value below costs no wait that would drain the prefetched tiles.
+      // Each turn of the ring loads tile t+p+R-1 into the slot tile t+p-1
+      // has just left, then processes tile t+p (all indices are constants
+      // after unrolling, so the ring lives in registers).
       int t = 0;
       do {
-        if constexpr (kRing<NB> == 3) {
-          const int r0 = row_of(t, c, cn);
-          const int r1 = row_of(t + 1, c, cn);
-          const int r2 = row_of(t + 2, c, cn);
-          load_tile<DK, DV, NB, CAUSAL>(t2, src, r2, last_row, i, k);
-          if (r0 <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(t0, r0, lim, k, lane, sh_q, m_run, l_run, acc);
-          load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(t + 3, c, cn), last_row, i, k);
-          if (r1 <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(t1, r1, lim, k, lane, sh_q, m_run, l_run, acc);
-          load_tile<DK, DV, NB, CAUSAL>(t1, src, row_of(t + 4, c, cn), last_row, i, k);
-          if (r2 <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(t2, r2, lim, k, lane, sh_q, m_run, l_run, acc);
-          t += 3;
-        } else {
-          const int r0 = row_of(t, c, cn);
-          const int r1 = row_of(t + 1, c, cn);
-          load_tile<DK, DV, NB, CAUSAL>(t1, src, r1, last_row, i, k);
-          if (r0 <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(t0, r0, lim, k, lane, sh_q, m_run, l_run, acc);
-          load_tile<DK, DV, NB, CAUSAL>(t0, src, row_of(t + 2, c, cn), last_row, i, k);
-          if (r1 <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(t1, r1, lim, k, lane, sh_q, m_run, l_run, acc);
-          t += 2;
+#pragma unroll
+        for (int p = 0; p < R; ++p) {
+          const int r = row_of(t + p, c, cn);
+          load_tile<DK, DV, NB, CAUSAL>(ring[(p + R - 1) % R], src, row_of(t + p + R - 1, c, cn),
+                                        last_row, i, k);
+          if (r <= last_row)
+            process_tile<DK, DV, NB, CAUSAL>(ring[p], r, lim, k, lane, sh_q, m_run, l_run, acc);
         }
+        t += R;
         // A wave whose remaining tiles all lie past the slab's end (only in the
         // slab's last chunk) leaves early instead of idling through them.
       } while (t < tpw && row_of(t, c, cn) <= last_row);
