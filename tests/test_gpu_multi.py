@@ -181,3 +181,56 @@ def test_multi_row_long_context_sampled(cuda_device):
                                 shape.scale32(), heads=heads)
             check(got[:, :, r][heads], ref[heads], f"spec4 step {t} row {r}")
         assert dl.cpu().numpy().tolist() == hl.tolist()
+
+
+def test_graph_replay_of_multi_row_steps(cuda_device):
+    """Two multi-row steps captured in one HIP graph, replayed three times
+    from the same initial cache with eager work in between."""
+    B, h_q, h_kv, n_max, d, T = 2, 16, 2, 600, 128, 4
+    shape = workloads.custom("graph_multi", B=B, h_q=h_q, h_kv=h_kv, d_k=d, d_v=d, n_max=n_max)
+    inp = workloads.make(shape, seed=31, lens=np.array([0, 597], np.int32))
+    dK0, dV0, dl0 = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
+    dK, dV, dl = dK0.clone(), dV0.clone(), dl0.clone()
+    qs = [rand(40 + t, (B, h_q, T, d)) for t in range(2)]
+    kns = [rand(50 + t, (B, h_kv, T, d)) for t in range(2)]
+    vns = [rand(60 + t, (B, h_kv, T, d)) for t in range(2)]
+    dq = [dev(x, cuda_device) for x in qs]
+    dkn = [dev(x, cuda_device) for x in kns]
+    dvn = [dev(x, cuda_device) for x in vns]
+    ws = binding.alloc_multi_workspace(dq[0], dK, dV)
+    outs = [torch.empty((B, h_q, T, d), device=cuda_device) for _ in range(2)]
+    scale = float(shape.scale32())
+    # the definition: single steps on the host mirror
+    hK, hV, hl = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    refs = []
+    for t in range(2):
+        ref = np.zeros((B, h_q, T, d))
+        for r in range(T):
+            oracle.append(hK, hV, np.ascontiguousarray(kns[t][:, :, r]),
+                          np.ascontiguousarray(vns[t][:, :, r]), hl)
+            ref[:, :, r] = oracle.decode(np.ascontiguousarray(qs[t][:, :, r]), hK, hV, hl,
+                                         shape.scale32())
+        refs.append(ref)
+    for t in range(2):   # eager pass first (loads the kernels)
+        binding.decode_multi_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=outs[t],
+                                  workspace=ws)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for t in range(2):
+            binding.decode_multi_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=outs[t],
+                                      workspace=ws)
+    for rep in range(3):
+        dK.copy_(dK0)
+        dV.copy_(dV0)
+        dl.copy_(dl0)
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        say(f"multi-row graph replay {rep}")
+        graph.replay()
+        torch.cuda.synchronize()
+        for t in range(2):
+            check(outs[t].cpu().numpy().astype(np.float64), refs[t], f"replay {rep} step {t}")
+        assert dl.cpu().numpy().tolist() == hl.tolist()
+        assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))

@@ -405,11 +405,14 @@ def test_single_step_workloads(cuda_device, name):
     check(got[sel], ref[sel], shape.name)
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["append_then_decode", "fused_step"])
 @pytest.mark.parametrize("name,check_steps,heads_per_b",
                          [("c2", None, 3), ("c5", (0, 1, 31, 62, 63), 2)])
-def test_multi_step_workloads(cuda_device, name, check_steps, heads_per_b):
-    """Append then decode, step after step, with len kept on the device; the
-    host mirror replays every append and the oracle checks sampled heads."""
+def test_multi_step_workloads(cuda_device, name, check_steps, heads_per_b, fused):
+    """Append then decode, step after step, with len kept on the device --
+    as two calls, or fused as the benchmark times it (the partial kernel with
+    the append, then the merge); the host mirror replays every append and the
+    oracle checks sampled heads."""
     shape = workloads.get(name)
     say(f"workload {shape.name}: generating inputs")
     inp = workloads.make(shape, seed=0)
@@ -421,11 +424,16 @@ def test_multi_step_workloads(cuda_device, name, check_steps, heads_per_b):
     out = torch.empty((shape.B, shape.h_q, shape.d_v), device=cuda_device)
     steps = range(shape.steps) if check_steps is None else check_steps
     for t in range(shape.steps):
-        binding.kv_append(dK, dV, dev(inp.k_new[t], cuda_device),
-                          dev(inp.v_new[t], cuda_device), dl)
-        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
         dq = dev(inp.q_step[t], cuda_device)
-        binding.decode_attn(dq, dK, dV, dl, float(shape.scale32()), out=out, workspace=ws)
+        kn, vn = dev(inp.k_new[t], cuda_device), dev(inp.v_new[t], cuda_device)
+        if fused:
+            binding.decode_partial(dq, dK, dV, dl, float(shape.scale32()), ws, k_new=kn, v_new=vn)
+            binding.decode_merge(out, ws, shape.B, shape.h_q, shape.h_kv, shape.n_max,
+                                 shape.d_k, shape.d_v, lens=dl)
+        else:
+            binding.kv_append(dK, dV, kn, vn, dl)
+            binding.decode_attn(dq, dK, dV, dl, float(shape.scale32()), out=out, workspace=ws)
+        oracle.append(hK, hV, inp.k_new[t], inp.v_new[t], hl)
         if t in steps:
             torch.cuda.synchronize()
             say(f"workload {shape.name}: step {t} check")
