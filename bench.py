@@ -238,7 +238,7 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not "
+        print(f"bench.py: this benchmark runs on one GPU; --gpus {args.gpus} is not "
               "supported (the decode would shard by KV head with no exchange, "
               "see the design notes)", file=sys.stderr)
         return 2
