@@ -57,7 +57,7 @@ typedef enum da_status {
     DA_ERR_NULL = 1,        /* a required pointer is NULL                          */
     DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q,
                                or chunk_rows not a positive multiple of 384        */
-    DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128} (decode), or not a
+    DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128, 256} (decode), or not a
                                multiple of 4 (append)                              */
     DA_ERR_ALIGN = 4,       /* a float array not 16-byte aligned, len not 4-byte   */
     DA_ERR_SCALE = 5,       /* scale is NaN or infinite                            */
@@ -123,7 +123,7 @@ size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
  * from call to call within fp32 rounding.  Equivalent to da_decode_partial
  * followed by da_decode_merge.
  *
- * Supported: d_k, d_v in {64, 128}; any B, h_q, h_kv >= 1 with h_kv | h_q.
+ * Supported: d_k, d_v in {64, 128, 256}; any B, h_q, h_kv >= 1 with h_kv | h_q.
  * workspace: see above; at least da_decode_workspace_bytes(...) bytes,
  * 16-byte aligned.  out must not overlap the inputs.
  */

@@ -66,16 +66,18 @@ constexpr int kComputeUnits = 256;                   // MI355X
 // per SIMD, whose registers fit without parking the accumulators in AGPRs and
 // whose second wave overlaps one wave's softmax with the other's products,
 // is 5 % (MQA) to 10 % (four query rows per head) faster.
-template <int NB>
-constexpr int kRing = NB == 2 ? 2 : 3;
-template <int NB>
-constexpr int kWavesPerSimd = NB == 2 ? 2 : 1;
+// A tile of d_k = d_v = 256 holds 128 registers per lane: such head sizes
+// take a two-tile ring at one wave per SIMD.
+template <int NB, int DK, int DV>
+constexpr int kRing = (NB == 2 || DK + DV > 256) ? 2 : 3;
+template <int NB, int DK, int DV>
+constexpr int kWavesPerSimd = (NB == 2 && DK + DV <= 256) ? 2 : 1;
 // A chunk is the rows a workgroup takes at a time: a multiple of six 16-row
 // tiles per wave (whole turns of either ring).  The default is 768 rows for
 // one column block and 384 for two, whose twice as many resident workgroups
 // need more chunks to share the tail (measured).
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
-static_assert(6 % kRing<1> == 0 && 6 % kRing<2> == 0, "chunks are whole turns of the ring");
+static_assert(6 % 2 == 0 && 6 % 3 == 0, "chunks are whole turns of either ring");
 constexpr int kDefaultChunkRows = 768;
 constexpr int kDefaultChunkRows2 = 384;
 // Visit slots per slab, in units of the even share of resident workgroups per
@@ -409,7 +411,7 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_kernel(
+__global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_partial_kernel(
     const float* __restrict__ q, float* __restrict__ K,
     float* __restrict__ V, const float* __restrict__ k_new,
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
@@ -609,7 +611,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd<NB>) void decode_partial_ke
                      : (cnn < nch ? cnn * C + (x - tpw) * (kWaves * kTileRows) + wave * kTileRows
                                   : last_row);
     };
-    constexpr int R = kRing<NB>;
+    constexpr int R = kRing<NB, DK, DV>;
     Tile<DK, DV, NB> ring[R];
 #pragma unroll
     for (int p = 0; p < R - 1; ++p)
@@ -843,7 +845,7 @@ struct Plan {
 };
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-bool dim_ok(int d) { return d == 64 || d == 128; }
+bool dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 size_t pad256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -877,8 +879,9 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   plan->single_chunk = chunks_per_slab == 1;
   // One resident workgroup per CU and wave slot, fewer if there are fewer
   // chunks than that.
-  const int64_t resident = (int64_t)kComputeUnits * (plan->blocks == 1 ? kWavesPerSimd<1>
-                                                                        : kWavesPerSimd<2>);
+  // (two waves per SIMD only for two column blocks at d_k + d_v <= 256)
+  const int64_t resident =
+      (int64_t)kComputeUnits * (plan->blocks == 2 && d_k + d_v <= 256 ? 2 : 1);
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
   // Every visit holds at least one chunk; kVisitSlack times the even share
   // of workgroups per slab leaves room for workgroups that move on from
@@ -995,8 +998,13 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
   (void)hipGetLastError();
   if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, a, w, s);
   else if (d_k == 64 && d_v == 128) launch_partial_nb<64, 128>(pl, a, w, s);
+  else if (d_k == 64 && d_v == 256) launch_partial_nb<64, 256>(pl, a, w, s);
   else if (d_k == 128 && d_v == 64) launch_partial_nb<128, 64>(pl, a, w, s);
-  else launch_partial_nb<128, 128>(pl, a, w, s);
+  else if (d_k == 128 && d_v == 128) launch_partial_nb<128, 128>(pl, a, w, s);
+  else if (d_k == 128 && d_v == 256) launch_partial_nb<128, 256>(pl, a, w, s);
+  else if (d_k == 256 && d_v == 64) launch_partial_nb<256, 64>(pl, a, w, s);
+  else if (d_k == 256 && d_v == 128) launch_partial_nb<256, 128>(pl, a, w, s);
+  else launch_partial_nb<256, 256>(pl, a, w, s);
   return launch_status();
 }
 
@@ -1018,7 +1026,11 @@ da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, in
   (void)hipGetLastError();
   const int heads_per_group = pl.blocks * kHeadsPerBlock;
   const dim3 grid((unsigned)pl.slabs * (unsigned)pl.merge_heads);
-  if (d_v == 64)
+  if (d_v == 256)
+    hipLaunchKernelGGL(decode_merge_kernel<256>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
+                       rows, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
+                       w.nvis, len_bump, n_max, T);
+  else if (d_v == 64)
     hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(kThreads), 0, s, out, w.ml, w.acc,
                        rows, h_kv, pl.head_groups, heads_per_group, pl.merge_heads, pl.J, w.cnt,
                        w.nvis, len_bump, n_max, T);

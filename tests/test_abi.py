@@ -51,7 +51,8 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     groups = -(-G // 32)
     slabs = B * h_kv * groups
     chunks = -(-n_max // c)
-    resident = 256 * (2 if G > 16 else 1)   # two waves per SIMD for two column blocks
+    # two waves per SIMD for two column blocks, unless the head sizes are large
+    resident = 256 * (2 if G > 16 and d_k + d_v <= 256 else 1)
     grid = max(1, min(resident, chunks * slabs))
     J = max(1, min(chunks, 4 * -(-grid // slabs)))
     slots = B * h_q * J
@@ -62,7 +63,8 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
 def test_chunk_rows_and_workspace_sizes():
     for args in [(1, 1, 1, 128, 64, 64), (8, 32, 32, 4112, 128, 128),
                  (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
-                 (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]:
+                 (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128),
+                 (2, 64, 2, 5000, 256, 256), (2, 16, 2, 900, 256, 64)]:
         c = binding.chunk_rows(*args)
         default = 384 if args[1] // args[2] > 16 else 768
         assert c == min(default, -(-args[3] // 384) * 384)
@@ -91,7 +93,7 @@ def _decode(**kw):
     (dict(B=0), 2), (dict(h_q=0), 2), (dict(h_kv=0), 2), (dict(n_max=0), 2),
     (dict(h_q=3, h_kv=2), 2), (dict(B=1 << 21), 2), (dict(chunk=100), 2),
     (dict(chunk=192), 2), (dict(chunk=-384), 2),
-    (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=256), 3),
+    (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=512), 3),
     (dict(q=FAKE + 4), 4), (dict(K=FAKE + 8), 4), (dict(out=FAKE + 4), 4),
     (dict(len=FAKE + 2), 4),
     (dict(scale=float("nan")), 5), (dict(scale=float("inf")), 5),

@@ -59,6 +59,7 @@ MULTI = [
     ("T16_two_groups", 1, 4, 1, 128, 128, 1000, 16, [1000]),
     ("dk128_dv64_T5_odd", 3, 6, 3, 128, 64, 97, 5, [97, 4, 60]),
     ("empty_and_short", 2, 8, 4, 128, 128, 70, 4, [0, 3]),
+    ("d256_T4", 2, 8, 2, 256, 256, 600, 4, [600, 2]),
 ]
 
 

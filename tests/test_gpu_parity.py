@@ -79,6 +79,10 @@ SMALL = [
     ("dk128_dv64", 2, 8, 4, 128, 64, 400, [15, 400]),
     ("g3_odd", 2, 9, 3, 64, 64, 97, [97, 2]),
     ("empty_and_full", 3, 8, 8, 128, 128, 70, [0, 70, 1]),
+    ("d256", 2, 8, 2, 256, 256, 900, [900, 33]),
+    ("d256_mqa_twoblocks", 1, 32, 1, 256, 256, 500, [500]),
+    ("dk256_dv64", 2, 4, 2, 256, 64, 300, [1, 300]),
+    ("dk64_dv256_g20", 2, 40, 2, 64, 256, 200, [200, 17]),
 ]
 
 
@@ -246,6 +250,7 @@ STEP_CASES = [
     ("mha_d64", 2, 4, 4, 64, 64, 300, [299, 300]),         # one full cache: no append
     ("mqa32_dkdv", 2, 32, 1, 64, 128, 200, [5, 190]),
     ("neg_len", 2, 8, 4, 128, 128, 100, [-3, 40]),
+    ("d256", 2, 8, 2, 256, 256, 400, [0, 399]),
 ]
 
 
