@@ -13,7 +13,7 @@ Functions follow the paper as follows:
   heads, with the psi-selection head map of eq. (10) for GQA/MQA.
 * :func:`decode_weights` -- Step II's weight vector for one (b, h).
 * :func:`append` -- the concatenation append of eqs. (6)-(7) with the
-  pre-allocated cache semantics of the "moa_kvcache" listing.
+  semantics of the multi-step section's pre-allocated cache.
 * :func:`decode_multi` -- T query rows per head with causal visibility (the
   rank-2 query of the paper's training form, for a step that submits several
   positions at once): each row is Algorithm 1 on its causal prefix.

@@ -10,8 +10,8 @@
  *
  * Arithmetic: inputs are fp32 as stored; every product, sum, max and exp is
  * done in fp64 (libm exp), results are fp64.  No blocking, fusion, online
- * softmax or reordering: each (batch, query head) follows Algorithm 1
- * ("MoA decode, single query step") in the paper's order -- all scores,
+ * softmax or reordering: each (batch, query head) follows Algorithm 1 (the
+ * single-query decode step of the DNF section) in the paper's order -- all scores,
  * then the max, then the exponentials, then Z, then the weights, then the
  * weighted sum.
  *
@@ -31,8 +31,9 @@
  *   - scale multiplies the dot product once, eq. (1); it is always passed in.
  *   - query head h reads KV head floor(h*h_kv/h_q), eq. (10) / Fig. 3.
  *   - rows used are 0 .. clamp(len[b],0,n_max)-1; an empty cache gives 0.
- *   - append writes row len[b] then increments len[b], Listing "moa_kvcache"
- *     semantics; at len[b] >= n_max (or len[b] < 0) it does nothing.
+ *   - append writes row len[b] then increments len[b] (the pre-allocated
+ *     cache of the multi-step section); at len[b] >= n_max (or len[b] < 0) it
+ *     does nothing.
  */
 #include <math.h>
 #include <stdint.h>
@@ -69,8 +70,8 @@ static void decode_one_query(const float *q, const float *Kslab,
 {
     if (n == 0) {
         /* Empty cache: Algorithm 1 has no rows to weight.  The result is
-         * defined as the zero vector (the reading the C listing's zeroed
-         * output buffer gives). */
+         * defined as the zero vector (what the paper's C kernel, which starts
+         * from a zeroed output, gives). */
         for (int d = 0; d < d_v; ++d) out[d] = 0.0;
         return;
     }

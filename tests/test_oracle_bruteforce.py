@@ -3,8 +3,8 @@
 The brute force takes another route to the same definition: Python
 ``decimal`` at 50 significant digits, the textbook softmax without the max
 subtraction, and the GQA head map by explicitly repeating each KV head
-G = h_q/h_kv times (the "repeat_interleave" expansion of the GQA section's
-standard listing) instead of computing the KV head index.
+G = h_q/h_kv times (the standard expansion the GQA section compares against)
+instead of computing the KV head index.
 """
 from decimal import Decimal, getcontext
 

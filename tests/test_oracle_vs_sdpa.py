@@ -80,7 +80,7 @@ def test_table5_gqa_vs_per_head_sdpa(h_kv):
     V = workloads.normal(2, 40 + h_kv, (1, h_kv, n, d))
     scale = np.float32(1.0 / math.sqrt(d))
     out = oracle.decode(q, K, V, np.array([n], np.int32), scale)[0]
-    Kx = np.repeat(K[0], G, axis=0)   # the standard listing's expansion
+    Kx = np.repeat(K[0], G, axis=0)   # the standard GQA expansion
     Vx = np.repeat(V[0], G, axis=0)
     ref64 = _sdpa(q[0][:, None], Kx, Vx, scale, torch.float64)[:, 0]
     ref32 = _sdpa(q[0][:, None], Kx, Vx, scale, torch.float32)[:, 0]
