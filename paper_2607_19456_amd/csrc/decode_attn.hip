@@ -80,9 +80,17 @@ constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 static_assert(6 % 2 == 0 && 6 % 3 == 0, "chunks are whole turns of either ring");
 constexpr int kDefaultChunkRows = 768;
 constexpr int kDefaultChunkRows2 = 384;
-// Visit slots per slab, in units of the even share of resident workgroups per
-// slab.
+// Visit slots per slab for dynamic visits, in units of the even share of
+// resident workgroups per slab.
 constexpr int kVisitSlack = 4;
+// Static share of each slab's rows, in sixteenths: the first
+// floor(14/16 * rows / C) chunks of every slab are divided among the
+// workgroups in advance, the rest is handed out dynamically in one-turn
+// chunks.  Sequences beyond kMaxStaticSeqs make the per-workgroup prefix
+// sums too long: such batches are scheduled dynamically only.
+constexpr int kStaticDen = 16;
+constexpr int kStaticNum = 14;
+constexpr int kMaxStaticSeqs = 256;
 constexpr int64_t kMaxSlabs = 1 << 20;
 constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
 // Each slab's scheduling word, {chunks taken (low half), visits opened (high
@@ -345,6 +353,102 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
   }
 }
 
+// ---------------------------------------------------------------------------
+// Static part of the schedule.
+//
+// Rows are scheduled in units of Cd rows (one turn of the tile ring for all
+// four waves).  Every slab of sequence b holds st(b) = floor(fnum/16 * n_b /
+// Cd) static units at its start; the rest of its rows is its dynamic part,
+// handed out one unit at a time.  The static units of all slabs, in slab
+// order, form one space of Ru units that is cut into gridDim.x contiguous
+// ranges, [w*Ru/G, (w+1)*Ru/G) for workgroup w: the ranges are proportional
+// to the rows, so every workgroup starts with the same amount of work (to
+// one unit) and without touching a counter.  A range covers one or more
+// slabs; each (workgroup, slab) pair is a visit with its own partial slot.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int static_units(int n_b, int Cd, int fnum) {
+  return (int)((int64_t)n_b * fnum / ((int64_t)kStaticDen * Cd));
+}
+
+// Units of the dynamic part of a slab with n rows.
+__device__ __forceinline__ int dynamic_units(int n, int Cd, int fnum) {
+  const int rest = n - static_units(n, Cd, fnum) * Cd;
+  return rest > 0 ? (rest + Cd - 1) / Cd : 0;
+}
+
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t v, int lane) {
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t o = __shfl_up(v, d);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Wave-wide (all 64 lanes).  Static units of one slab of sequence `bq` and
+// of one slab of each sequence before it; returns the static units of one
+// slab summed over all sequences.
+__device__ int64_t static_scan(const int32_t* __restrict__ len, int B, int n_max, bool app, int T,
+                               int Cd, int fnum, int bq, int lane, int64_t* before, int* st_bq) {
+  int64_t carry = 0;
+  for (int b0 = 0; b0 < B; b0 += kWave) {
+    const int b = b0 + lane;
+    const int64_t v = b < B ? static_units(decode_rows(len[b], n_max, app, T), Cd, fnum) : 0;
+    const int64_t incl = wave_incl_scan(v, lane);
+    if (bq >= b0 && bq < b0 + kWave) {
+      *before = carry + __shfl(incl - v, bq - b0);
+      *st_bq = (int)__shfl(v, bq - b0);
+    }
+    carry += __shfl(incl, kWave - 1);
+  }
+  return carry;
+}
+
+// Wave-wide.  The sequence whose slabs hold static unit u (a sequence holds
+// per_b times the static units of one of its slabs); *first = its first
+// unit, *st = its static units per slab.  -1 if u lies beyond every static
+// unit.
+__device__ int static_locate(const int32_t* __restrict__ len, int B, int n_max, bool app, int T,
+                             int Cd, int fnum, int per_b, int64_t u, int lane, int64_t* first,
+                             int* st) {
+  int64_t carry = 0;
+  for (int b0 = 0; b0 < B; b0 += kWave) {
+    const int b = b0 + lane;
+    const int64_t v =
+        b < B ? (int64_t)per_b * static_units(decode_rows(len[b], n_max, app, T), Cd, fnum) : 0;
+    const int64_t incl = wave_incl_scan(v, lane);
+    const unsigned long long m = __ballot(carry + incl > u);
+    if (m) {
+      const int f = __ffsll((long long)m) - 1;
+      *first = carry + __shfl(incl - v, f);
+      *st = (int)(__shfl(v, f) / per_b);
+      return b0 + f;
+    }
+    carry += __shfl(incl, kWave - 1);
+  }
+  return -1;
+}
+
+__device__ __forceinline__ int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Static visits (= partial slots) of a slab whose static units are units
+// [Ps, Ps + st) of Ru, cut G ways.  With Ru >= G every workgroup whose range
+// meets the slab has a slot, numbered from the first such workgroup; with
+// Ru < G every range is at most one unit and the slot is the unit's index in
+// the slab (workgroups with an empty range take none).
+__device__ __forceinline__ int static_visits(int64_t Ps, int st, int64_t Ru, int G) {
+  if (st <= 0) return 0;
+  if (Ru < G) return st;
+  const int64_t wf = ceil_div64((Ps + 1) * G, Ru) - 1;
+  const int64_t wl = ceil_div64((Ps + st) * G, Ru) - 1;
+  return (int)(wl - wf + 1);
+}
+
+__device__ __forceinline__ int static_slot(int64_t Ps, int64_t u, int64_t Ru, int G, int w) {
+  if (Ru < G) return (int)(u - Ps);
+  return (int)(w - (ceil_div64((Ps + 1) * G, Ru) - 1));
+}
+
 // Number of cache rows of slab s = (b, KV head, head group).
 __device__ __forceinline__ int slab_rows(const int32_t* __restrict__ len, int s, int per_b,
                                          int n_max, bool app, int T) {
@@ -356,20 +460,20 @@ __device__ __forceinline__ unsigned long long load_word(const unsigned long long
 }
 
 // Wave-wide search (all 64 lanes call it): the first slab at or after
-// `start` (cyclically) that still has chunks and visit slots left, looking
+// `start` (cyclically) that still has dynamic chunks and visit slots left, looking
 // at no more than `budget` slabs.  Returns -1 if none; *seen is the number of
 // slabs examined up to and including the one returned.
 __device__ int find_open_slab(const unsigned* __restrict__ cnt,
                               const int32_t* __restrict__ len, int start, int budget, int S,
-                              int per_b, int n_max, bool app, int T, int C, int J, int lane,
-                              int* seen) {
+                              int per_b, int n_max, bool app, int T, int Cd, int fnum,
+                              int J, int lane, int* seen) {
   for (int base = 0; base < budget; base += kWave) {
     const int o = base + lane;
     int sl = start + o;
     if (sl >= S) sl -= S;
     bool open = false;
     if (o < budget) {
-      const int nch = (slab_rows(len, sl, per_b, n_max, app, T) + C - 1) / C;
+      const int nch = dynamic_units(slab_rows(len, sl, per_b, n_max, app, T), Cd, fnum);
       const unsigned long long w = load_word(
           reinterpret_cast<const unsigned long long*>(cnt + (size_t)sl * kCounterStride));
       open = (unsigned)w < (unsigned)nch && (unsigned)(w >> 32) < (unsigned)J;
@@ -415,13 +519,12 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
     const float* __restrict__ q, float* __restrict__ K,
     float* __restrict__ V, const float* __restrict__ k_new,
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
-    int B, int h_q, int h_kv, int n_max, int T, int C, int head_groups, int J,
-    unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
+    int B, int h_q, int h_kv, int n_max, int T, int C, int Cd, int fnum, int head_groups, int J,
+    int Jd, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
     float* __restrict__ ws_acc, float* __restrict__ out_direct) {
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
-  const int tpw = C / (kTileRows * kWaves);             // tiles per wave per chunk
   const bool app = k_new != nullptr;                    // fused append (eqs. (6)-(7))
 
   const int tid = threadIdx.x;
@@ -430,8 +533,8 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
   const int i = lane & 15;
   const int k = lane >> 4;
 
-  __shared__ int sh_ctl[4];                             // slab, visit slot, chunk, next chunk
-  __shared__ int sh_next[2];                            // chunk after next, by parity
+  __shared__ int sh_ctl[7];      // slab, slot, first static chunk, static chunks, d0, d1, dynamic
+  __shared__ int sh_next[2];     // dynamic chunk after next, by parity
   __shared__ f4 sh_q[NB][DK / 16][kWave];
   __shared__ f4 sh_acc[kWaves - 1][NB][DV / 64][4][kWave];
   __shared__ float sh_m[kWaves - 1][NB][kWave];
@@ -467,36 +570,93 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
   // owns slab s, takes its one chunk without searching and writes the output
   // rows itself -- no merge, and no other workgroup touches its counter line.
   bool first = true;
+  // This workgroup's static range, units [u_lo, u_hi) of Ru (wave 0 only).
+  // Ranges go by rank.  With two resident workgroups per CU (two waves per
+  // SIMD) workgroups w and w + 256 share a CU, and the older one's waves win
+  // the issue arbitration, so it runs markedly faster: ranking them next to
+  // each other puts both kinds on every slab, where the faster ones drain
+  // the slab's dynamic part.
+  const int Gw = (int)gridDim.x;
+  const int rank = Gw == 2 * kComputeUnits
+                       ? (int)(blockIdx.x % kComputeUnits) * 2 + (int)(blockIdx.x / kComputeUnits)
+                       : (int)blockIdx.x;
+  int64_t Ru = 0, u_lo = 0, u_hi = 0;
+  if (wave == 0 && fnum > 0) {
+    int64_t before;
+    int st;
+    Ru = (int64_t)per_b * static_scan(len, B, n_max, app, T, Cd, fnum, -1, lane, &before, &st);
+    u_lo = (int64_t)rank * Ru / Gw;
+    u_hi = (int64_t)(rank + 1) * Ru / Gw;
+  }
 
   while (true) {
-    // ---- wave 0 opens a visit: a slab with chunks and slots left.  Lane 0
-    // takes the slot and the first two chunks with one compare-and-swap on
-    // the slab's {chunks, visits} word, so every visit has at least one
-    // chunk and there are never more than J of them.
+    // ---- wave 0 opens a visit.  First the static visits of this
+    // workgroup's range, one per slab the range meets; the last of them (the
+    // home visit) goes on with the dynamic chunks of its slab.  Then dynamic
+    // visits on any slab with dynamic chunks and slots left: lane 0 takes the
+    // slot and the first two chunks with one compare-and-swap on the slab's
+    // {chunks, visits} word, so every such visit has at least one chunk and
+    // no slab gets more than Jd of them.
     if (wave == 0) {
-      int s = -1, j = -1, c = -1, cn = -1;
+      int s = -1, j = -1, sr = 0, er = 0, d0 = -1, d1 = -1, dyn = 0;
       int budget = out_direct ? 0 : S;
-      if (out_direct && first) {
-        s = blockIdx.x;
-        j = 0;
-        c = 0;
-        cn = 1;
+      if (out_direct) {
+        if (first) {
+          s = blockIdx.x;
+          j = 0;
+          er = C;
+        }
+      } else if (u_lo < u_hi) {
+        int64_t fu = 0;
+        int stb = 0;
+        const int bs =
+            static_locate(len, B, n_max, app, T, Cd, fnum, per_b, u_lo, lane, &fu, &stb);
+        if (bs >= 0 && stb > 0) {
+          const int r = (int)((u_lo - fu) / stb);
+          const int64_t Ps = fu + (int64_t)r * stb;
+          const int64_t e = u_hi < Ps + stb ? u_hi : Ps + stb;
+          s = bs * per_b + r;
+          j = static_slot(Ps, u_lo, Ru, Gw, rank);
+          sr = (int)(u_lo - Ps) * Cd;
+          er = (int)(e - Ps) * Cd;
+          u_lo = e;
+          budget = 0;
+          if (u_lo == u_hi) {
+            // The home visit.  If its static rows do not fill the
+            // two-segment window, its first dynamic units are taken now.
+            dyn = 1;
+            start = s;
+            const int nseg = (er - sr + C - 1) / C;
+            if (nseg < 2) {
+              unsigned long long got = 0;
+              if (lane == 0)
+                got = atomicAdd(
+                    reinterpret_cast<unsigned long long*>(cnt + (size_t)s * kCounterStride),
+                    (unsigned long long)(2 - nseg));
+              got = __shfl(got, 0);
+              d0 = (int)(unsigned)got;
+              d1 = d0 + 1;
+            }
+          }
+        } else {
+          u_lo = u_hi;
+        }
       }
       while (budget > 0) {
         int seen;
-        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, T, C, J,
-                                        lane, &seen);
+        const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, T, Cd,
+                                        fnum, Jd, lane, &seen);
         if (cand < 0) break;
         budget -= seen;
         start = cand + 1 == S ? 0 : cand + 1;
-        const int nch = (slab_rows(len, cand, per_b, n_max, app, T) + C - 1) / C;
+        const int nch = dynamic_units(slab_rows(len, cand, per_b, n_max, app, T), Cd, fnum);
         unsigned long long got = ~0ull;
         if (lane == 0) {
           unsigned long long* w =
               reinterpret_cast<unsigned long long*>(cnt + (size_t)cand * kCounterStride);
           unsigned long long old = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           // Lock-free: a failed swap means another workgroup moved the word.
-          while ((unsigned)old < (unsigned)nch && (unsigned)(old >> 32) < (unsigned)J) {
+          while ((unsigned)old < (unsigned)nch && (unsigned)(old >> 32) < (unsigned)Jd) {
             const unsigned long long seen_w = atomicCAS(w, old, old + (1ull << 32) + 2ull);
             if (seen_w == old) {
               got = old;
@@ -508,18 +668,38 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
         got = __shfl(got, 0);
         if (got == ~0ull) continue;                     // no chunk or slot left meanwhile
         s = cand;
-        j = (int)(got >> 32);
-        c = (int)(unsigned)got;
-        cn = c + 1;
+        d0 = (int)(unsigned)got;
+        d1 = d0 + 1;
+        dyn = 1;
+        // Dynamic slots follow the slab's static ones.
+        int base = 0;
+        if (fnum > 0) {
+          int64_t before = 0;
+          int st = 0;
+          static_scan(len, B, n_max, app, T, Cd, fnum, cand / per_b, lane, &before, &st);
+          base = static_visits((int64_t)per_b * before + (int64_t)(cand % per_b) * st, st, Ru, Gw);
+        }
+        j = base + (int)(got >> 32);
         break;
       }
-      if (lane == 0) { sh_ctl[0] = s; sh_ctl[1] = j; sh_ctl[2] = c; sh_ctl[3] = cn; }
+      if (lane == 0) {
+        sh_ctl[0] = s;
+        sh_ctl[1] = j;
+        sh_ctl[2] = sr;
+        sh_ctl[3] = er;
+        sh_ctl[4] = d0;
+        sh_ctl[5] = d1;
+        sh_ctl[6] = dyn;
+      }
     }
     __syncthreads();
     const int s = sh_ctl[0];
     const int j = sh_ctl[1];
-    int c = sh_ctl[2];
-    int cn = sh_ctl[3];
+    const int sr = sh_ctl[2];
+    const int er = sh_ctl[3];
+    const int d0 = sh_ctl[4];
+    const int d1 = sh_ctl[5];
+    const bool dyn = sh_ctl[6] != 0;
     if (s < 0) break;                                   // every slab is exhausted
     first = false;
 
@@ -529,9 +709,8 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
     const int hgrp = rem - g * head_groups;
     const int32_t len_b = len[b];
     const int n = decode_rows(len_b, n_max, app, T);
-    const int nch = (n + C - 1) / C;
     const int last_row = n - 1;
-    if (out_direct && nch == 0) {
+    if (out_direct && n == 0) {
       // An empty cache: the slab's output rows are zero.
       const int hc = min(NB * kHeadsPerBlock, G - hgrp * (NB * kHeadsPerBlock));
       float* o = out_direct + ((int64_t)b * h_q + g * G + hgrp * (NB * kHeadsPerBlock)) * DV;
@@ -599,55 +778,99 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
         for (int e = 0; e < 4; ++e) acc[nb][cc][e] = f4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // The wave's tiles of chunk x: rows x*C + (4t + wave)*16, t < tpw.  The
-    // register tiles form a ring: while one tile is on the matrix cores the
-    // loads of the next R-1 are in flight, across chunk boundaries
-    // too (tile x of the wave's sequence: x < tpw in this chunk, then the next
-    // chunk's; past the visit's end the clamped last row, already cached, is
-    // loaded so every path keeps the same loads in flight).  The chunk after
-    // next is requested at the start of each chunk.
-    auto row_of = [&](int x, int cc, int cnn) {
-      return x < tpw ? cc * C + x * (kWaves * kTileRows) + wave * kTileRows
-                     : (cnn < nch ? cnn * C + (x - tpw) * (kWaves * kTileRows) + wave * kTileRows
-                                  : last_row);
+    // The visit's rows are a stream of segments: its static rows [sr, er)
+    // in segments of up to C rows, then, for the home visit and dynamic
+    // visits, the slab's dynamic units in the order its counter hands them
+    // out (Cd rows each, from row srows on).  The workgroup always knows the
+    // current segment (start row cs, ctpw tiles per wave) and the next one
+    // (ns < 0: none); a dynamic segment after next is requested at the start
+    // of each segment.  A wave's tiles of a segment start at rows cs + x*64 +
+    // wave*16, x < ctpw.  The register tiles form a ring: while one tile is
+    // on the matrix cores the loads of the next R-1 are in flight, across
+    // segment boundaries too (past the visit's end the clamped last row,
+    // already cached, is loaded so every path keeps the same loads in flight).
+    constexpr int kRowsPerTurn = kWaves * kTileRows;
+    const int srows = static_units(n, Cd, fnum) * Cd;
+    const int nchd = dynamic_units(n, Cd, fnum);
+    const int tpw_d = Cd / kRowsPerTurn;
+    auto dyn_row = [&](int d) { return d >= 0 && d < nchd ? srows + d * Cd : -1; };
+    auto static_tpw = [&](int at) { return min(C, er - at) / kRowsPerTurn; };
+    int snext = sr;                                     // next static segment not yet entered
+    int cs, ctpw, ns, ntpw;
+    bool d0_used = false;
+    if (snext < er) {
+      cs = snext;
+      ctpw = static_tpw(snext);
+      snext += C;
+    } else {
+      cs = dyn ? dyn_row(d0) : -1;
+      ctpw = tpw_d;
+      d0_used = true;
+    }
+    if (snext < er) {
+      ns = snext;
+      ntpw = static_tpw(snext);
+      snext += C;
+    } else {
+      ns = dyn ? dyn_row(d0_used ? d1 : d0) : -1;
+      ntpw = tpw_d;
+    }
+    auto row_of = [&](int x) {
+      return x < ctpw ? cs + x * kRowsPerTurn + wave * kTileRows
+                      : (ns >= 0 ? ns + (x - ctpw) * kRowsPerTurn + wave * kTileRows : last_row);
     };
     constexpr int R = kRing<NB, DK, DV>;
-    Tile<DK, DV, NB> ring[R];
+    if (cs >= 0) {
+      Tile<DK, DV, NB> ring[R];
 #pragma unroll
-    for (int p = 0; p < R - 1; ++p)
-      load_tile<DK, DV, NB, CAUSAL>(ring[p], src, row_of(p, c, cn), last_row, i, k);
-    for (int it = 0;; ++it) {
-      // Thread 0 asks for the chunk after next even on the last chunk (the
-      // counter simply runs past the end): a conditional request would merge
-      // its result with another value right here and force a wait for it.
-      int after;
-      if (tid == 0) after = (int)(unsigned)atomicAdd(slab_word, 1ull);
-      // A loop that always runs at least once and exits at its bottom: after
-      // its first wait on a tile load the compiler knows the atomic issued
-      // above (an older memory operation) has returned, so publishing its
-      // value below costs no wait that would drain the prefetched tiles.
-      // Each turn of the ring loads tile t+p+R-1 into the slot tile t+p-1
-      // has just left, then processes tile t+p (all indices are constants
-      // after unrolling, so the ring lives in registers).
-      int t = 0;
-      do {
+      for (int p = 0; p < R - 1; ++p)
+        load_tile<DK, DV, NB, CAUSAL>(ring[p], src, row_of(p), last_row, i, k);
+      for (int it = 0;; ++it) {
+        // The segment after next comes from the counter once the static
+        // rows are all in the window.  Its value is left undefined for the
+        // threads that do not ask (rather than merged with a default): a
+        // merge right here would make the compiler wait for the request, and
+        // with it for every prefetched tile load.
+        const bool req = dyn && ns >= 0 && snext >= er;
+        int after;
+        if (tid == 0 && req) after = (int)(unsigned)atomicAdd(slab_word, 1ull);
+        // A loop that always runs at least once and exits at its bottom:
+        // after its first wait on a tile load the compiler knows the request
+        // issued above (an older memory operation) has returned, so
+        // publishing its value below costs no wait that would drain the
+        // prefetched tiles.  Each turn of the ring loads tile t+p+R-1 into
+        // the slot tile t+p-1 has just left, then processes tile t+p (all
+        // indices are constants after unrolling, so the ring lives in
+        // registers).
+        int t = 0;
+        do {
 #pragma unroll
-        for (int p = 0; p < R; ++p) {
-          const int r = row_of(t + p, c, cn);
-          load_tile<DK, DV, NB, CAUSAL>(ring[(p + R - 1) % R], src, row_of(t + p + R - 1, c, cn),
-                                        last_row, i, k);
-          if (r <= last_row)
-            process_tile<DK, DV, NB, CAUSAL>(ring[p], r, lim, k, lane, sh_q, m_run, l_run, acc);
+          for (int p = 0; p < R; ++p) {
+            const int r = row_of(t + p);
+            load_tile<DK, DV, NB, CAUSAL>(ring[(p + R - 1) % R], src, row_of(t + p + R - 1),
+                                          last_row, i, k);
+            if (r <= last_row)
+              process_tile<DK, DV, NB, CAUSAL>(ring[p], r, lim, k, lane, sh_q, m_run, l_run, acc);
+          }
+          t += R;
+          // A wave whose remaining tiles all lie past the slab's end (only
+          // in the slab's last chunk) leaves early instead of idling through
+          // them.
+        } while (t < ctpw && row_of(t) <= last_row);
+        if (tid == 0 && req) sh_next[it & 1] = after;
+        __syncthreads();
+        cs = ns;
+        ctpw = ntpw;
+        if (cs < 0) break;
+        if (snext < er) {
+          ns = snext;
+          ntpw = static_tpw(snext);
+          snext += C;
+        } else {
+          ns = req ? dyn_row(sh_next[it & 1]) : -1;
+          ntpw = tpw_d;
         }
-        t += R;
-        // A wave whose remaining tiles all lie past the slab's end (only in the
-        // slab's last chunk) leaves early instead of idling through them.
-      } while (t < tpw && row_of(t, c, cn) <= last_row);
-      if (tid == 0) sh_next[it & 1] = after;
-      __syncthreads();
-      if (cn >= nch) break;
-      c = cn;
-      cn = sh_next[it & 1];
+      }
     }
 
     // Row sums of head i are spread over the 4 row groups k.
@@ -833,12 +1056,15 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
 // Host side: validation, sizing, launches.
 // ---------------------------------------------------------------------------
 struct Plan {
-  int chunk_rows;     // rows per dynamically scheduled chunk
+  int chunk_rows;     // rows per static chunk
+  int dyn_rows;       // rows per dynamic chunk (one ring turn of the 4 waves)
+  int fnum;           // static share of the rows, in sixteenths (0: all dynamic)
   int head_groups;    // groups of up to 32 query heads per KV head
   int blocks;         // MFMA column blocks per wave (1 or 2)
   int slabs;          // B * h_kv * head_groups
   int grid;           // resident workgroups of the partial kernel
-  int J;              // visit slots per (b, query head)
+  int J;              // visit slots per (b, query head): static, then dynamic
+  int Jd;             // dynamic visit slots per slab
   int merge_heads;    // query heads per slab the merge covers
   bool single_chunk;  // every slab fits in one chunk (direct form possible)
   size_t line_bytes, counter_bytes, ml_bytes, bytes;
@@ -883,11 +1109,23 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int64_t resident =
       (int64_t)kComputeUnits * (plan->blocks == 2 && d_k + d_v <= 256 ? 2 : 1);
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
-  // Every visit holds at least one chunk; kVisitSlack times the even share
-  // of workgroups per slab leaves room for workgroups that move on from
-  // finished slabs.
+  // Static share: off for single-chunk caches (direct form) and for batches
+  // whose per-workgroup prefix over sequences would be long.
+  plan->fnum = (!plan->single_chunk && B <= kMaxStaticSeqs) ? kStaticNum : 0;
+  // Scheduling units (static ranges and dynamic hand-outs) are one ring turn
+  // of the four waves when there is a static share, else whole chunks.
+  const int ring = (plan->blocks == 2 || d_k + d_v > 256) ? 2 : 3;
+  plan->dyn_rows = plan->fnum > 0 ? ring * kWaves * kTileRows : chunk_rows;
+  // Static slots: at most one per static unit of a slab plus one, and never
+  // more than the workgroups.  Dynamic slots: every dynamic visit holds at
+  // least one chunk; kVisitSlack times the even share of workgroups per slab
+  // leaves room for workgroups that move on from finished slabs.
+  const int64_t Js =
+      plan->fnum > 0 ? std::min<int64_t>(plan->grid, ceil_div(n_max, plan->dyn_rows)) + 1 : 0;
   const int64_t share = ceil_div((int64_t)plan->grid, plan->slabs);
-  plan->J = (int)std::max<int64_t>(1, std::min(chunks_per_slab, kVisitSlack * share));
+  plan->Jd = (int)std::max<int64_t>(
+      1, std::min(ceil_div(n_max, plan->dyn_rows), kVisitSlack * share));
+  plan->J = (int)(Js + plan->Jd);
   const size_t heads = (size_t)B * h_q;
   const size_t slots = heads * plan->J;
   plan->line_bytes = pad256((size_t)plan->slabs * kCounterStride * sizeof(unsigned));
@@ -935,9 +1173,11 @@ template <int DK, int DV, int NB, bool CAUSAL>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
   // The direct form runs one workgroup per slab; otherwise the resident grid.
   const unsigned grid = a.out_direct ? (unsigned)pl.slabs : (unsigned)pl.grid;
+  // The direct form schedules nothing: no static share.
   hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL>), dim3(grid), dim3(kThreads),
                      0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
-                     a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.head_groups, pl.J, w.cnt, w.nvis,
+                     a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.dyn_rows,
+                     a.out_direct ? 0 : pl.fnum, pl.head_groups, pl.J, pl.Jd, w.cnt, w.nvis,
                      w.ml, w.acc, a.out_direct);
 }
 

@@ -43,9 +43,15 @@ def test_status_strings():
 
 
 def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
-    """The sizing rule, restated: one visit slot per (b, query head) for up to
-    4x the even share of resident workgroups per slab; one 128-byte counter
-    line per slab and one visit count per (b, query head)."""
+    """The sizing rule, restated: rows are scheduled in units of one ring
+    turn (64 rows per tile of the ring: 3 tiles, or 2 for two column blocks
+    or large heads); per (b, query head) one visit slot for each static
+    visit a slab can have (at most one per unit plus one, and at most one per
+    resident workgroup) and, for dynamic visits, up to 4x the even share of
+    resident workgroups per slab (at most one per unit); one 128-byte
+    counter line per slab and one visit count per (b, query head).
+    Single-chunk caches and batches of more than 256 sequences are scheduled
+    dynamically only, in whole chunks."""
     pad = lambda x: -(-x // 256) * 256
     G = h_q // h_kv
     groups = -(-G // 32)
@@ -54,7 +60,12 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     # two waves per SIMD for two column blocks, unless the head sizes are large
     resident = 256 * (2 if G > 16 and d_k + d_v <= 256 else 1)
     grid = max(1, min(resident, chunks * slabs))
-    J = max(1, min(chunks, 4 * -(-grid // slabs)))
+    static = chunks > 1 and B <= 256
+    ring = 2 if G > 16 or d_k + d_v > 256 else 3
+    dyn_rows = ring * 64 if static else c
+    Js = min(grid, -(-n_max // dyn_rows)) + 1 if static else 0
+    Jd = max(1, min(-(-n_max // dyn_rows), 4 * -(-grid // slabs)))
+    J = Js + Jd
     slots = B * h_q * J
     counters = pad(slabs * 128) + pad(B * h_q * 4)
     return counters, counters + pad(slots * 8) + slots * d_v * 4
