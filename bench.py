@@ -52,11 +52,15 @@ def log(msg):
 
 def kernel_build_hash() -> str:
     """sha256 of the kernel source and the compiler flags it is built with
-    (either changes the code the counters were taken on)."""
+    (either changes the code the counters were taken on).  Paths in the
+    flags are taken relative to the repository, so the hash does not depend
+    on where the checkout lives."""
     from paper_2607_19456_amd import build
     with open(KERNEL_SRC, "rb") as f:
         src = f.read()
-    return hashlib.sha256(src + "\n".join(build.FLAGS).encode()).hexdigest()
+    flags = ["-I" + os.path.relpath(f[2:], ROOT) if f.startswith("-I") else f
+             for f in build.FLAGS]
+    return hashlib.sha256(src + "\n".join(flags).encode()).hexdigest()
 
 
 def counter_traffic(workload: str):

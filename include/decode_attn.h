@@ -83,8 +83,9 @@ const char *da_status_string(int status);
  */
 
 /*
- * Rows per work chunk the library picks for these shapes when chunk_rows is
- * 0 below (a positive multiple of 384).  Returns 0 if the shapes are invalid.
+ * Rows per work segment the library picks for these shapes when chunk_rows
+ * is 0 below (a positive multiple of 384).  Returns 0 if the shapes are
+ * invalid.
  */
 int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
 
@@ -114,14 +115,18 @@ size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
  * n_b = 0 gives out[b,h,:] = 0.  `scale` is applied once to the dot product
  * (the caller passes 1/sqrt(d_k) for standard attention).
  *
- * Each (b, KV head) slab's rows are cut into chunks of chunk_rows rows (0 =
- * the library's choice) that a resident set of workgroups takes dynamically;
- * a workgroup folds every chunk it takes from one slab into one running
- * softmax state (the online form of eq. (2)) and leaves one partial per
- * visit; a second launch combines the partials exactly (a regrouping of eqs.
- * (2)-(3) over disjoint row sets).  The summation order therefore varies
- * from call to call within fp32 rounding.  Equivalent to da_decode_partial
- * followed by da_decode_merge.
+ * A resident set of workgroups shares the rows of all (b, KV head) slabs:
+ * most of each slab in row ranges fixed in advance (proportional to the
+ * lengths), the rest in small units handed out dynamically; a workgroup reads
+ * its rows in segments of up to chunk_rows rows (0 = the library's choice),
+ * folds everything it reads from one slab into one running softmax state
+ * (the online form of eq. (2)) and leaves one partial per visit; a second
+ * launch combines the partials exactly (a regrouping of eqs. (2)-(3) over
+ * disjoint row sets).  Which workgroup takes which dynamic unit varies, so
+ * the summation order varies from call to call within fp32 rounding.  When
+ * every slab fits in one segment the decode is a single launch that writes
+ * out directly.  Equivalent to da_decode_partial followed by
+ * da_decode_merge.
  *
  * Supported: d_k, d_v in {64, 128, 256}; any B, h_q, h_kv >= 1 with h_kv | h_q.
  * workspace: see above; at least da_decode_workspace_bytes(...) bytes,

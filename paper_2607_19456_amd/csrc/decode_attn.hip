@@ -18,9 +18,11 @@
 //                          and resets the scheduling state.
 //
 // Work decomposition of decode_partial_kernel
-//   A resident grid of 256-thread workgroups (4 waves) takes chunks of slab
-//   rows dynamically; a workgroup's waves take the chunk's 16-row tiles
-//   round-robin.  Each tile is two dense products on the matrix cores
+//   A resident grid of 256-thread workgroups (4 waves) shares the slabs' rows:
+//   most of each slab in ranges fixed in advance, proportional to the
+//   lengths, the rest in small units handed out by per-slab counters; a
+//   workgroup's waves take each segment's 16-row tiles round-robin.  Each
+//   tile is two dense products on the matrix cores
 //   (v_mfma_f32_16x16x4_f32, fp32 in and out):
 //     scores  S[16 rows x 16 heads] = K_tile[16 x d_k] . Q^T[d_k x 16]
 //     update  O^T[d_v x 16 heads]  += V_tile^T[d_v x 16] . P[16 x 16 heads]
@@ -72,10 +74,11 @@ template <int NB, int DK, int DV>
 constexpr int kRing = (NB == 2 || DK + DV > 256) ? 2 : 3;
 template <int NB, int DK, int DV>
 constexpr int kWavesPerSimd = (NB == 2 && DK + DV <= 256) ? 2 : 1;
-// A chunk is the rows a workgroup takes at a time: a multiple of six 16-row
-// tiles per wave (whole turns of either ring).  The default is 768 rows for
-// one column block and 384 for two, whose twice as many resident workgroups
-// need more chunks to share the tail (measured).
+// A segment (chunk_rows) is the most rows a workgroup reads in one go from
+// its static range, a multiple of six 16-row tiles per wave (whole turns of
+// either ring); with no static share (single-chunk caches, very large
+// batches) it is also the unit handed out dynamically.  The default is 768
+// rows for one column block and 384 for two (measured).
 constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
 static_assert(6 % 2 == 0 && 6 % 3 == 0, "chunks are whole turns of either ring");
 constexpr int kDefaultChunkRows = 768;
@@ -84,18 +87,19 @@ constexpr int kDefaultChunkRows2 = 384;
 // resident workgroups per slab.
 constexpr int kVisitSlack = 4;
 // Static share of each slab's rows, in sixteenths: the first
-// floor(14/16 * rows / C) chunks of every slab are divided among the
-// workgroups in advance, the rest is handed out dynamically in one-turn
-// chunks.  Sequences beyond kMaxStaticSeqs make the per-workgroup prefix
-// sums too long: such batches are scheduled dynamically only.
+// floor(14/16 * rows / Cd) units of Cd rows (one turn of the tile ring) of
+// every slab are divided among the workgroups in advance, the rest is handed
+// out dynamically one unit at a time.  Batches of more than kMaxStaticSeqs
+// sequences would make the per-workgroup prefix sums long: they are
+// scheduled dynamically only.
 constexpr int kStaticDen = 16;
 constexpr int kStaticNum = 14;
 constexpr int kMaxStaticSeqs = 256;
 constexpr int64_t kMaxSlabs = 1 << 20;
 constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
-// Each slab's scheduling word, {chunks taken (low half), visits opened (high
-// half)}, has a 128-byte line of its own, so atomics on different slabs'
-// words never serialize on the same line.
+// Each slab's scheduling word, {dynamic units taken (low half), dynamic
+// visits opened (high half)}, has a 128-byte line of its own, so atomics on
+// different slabs' words never serialize on the same line.
 constexpr int kCounterStride = 32;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -460,7 +464,7 @@ __device__ __forceinline__ unsigned long long load_word(const unsigned long long
 }
 
 // Wave-wide search (all 64 lanes call it): the first slab at or after
-// `start` (cyclically) that still has dynamic chunks and visit slots left, looking
+// `start` (cyclically) that still has dynamic units and visit slots left, looking
 // at no more than `budget` slabs.  Returns -1 if none; *seen is the number of
 // slabs examined up to and including the one returned.
 __device__ int find_open_slab(const unsigned* __restrict__ cnt,
@@ -493,23 +497,26 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 // ---------------------------------------------------------------------------
 // Partials, persistent form.
 //
-// A slab is the cache rows of one (b, KV head, head group); it is cut into
-// chunks of C rows handed out by a per-slab counter.  A fixed set of
-// workgroups (one per CU and wave slot) stays resident; each one opens a
-// "visit" on a slab with chunks left (taking, in one atomic step, its first
-// two chunks and a visit slot j < J, so every visit has rows and the slots in
-// use are exactly 0 .. visits-1), takes chunks from that slab's counter until
-// none are left -- its four waves interleave the chunk's 16-row tiles, so the
-// workgroup streams one contiguous run of K and of V -- and folds all of them
-// into one running (max, sum, weighted sum) state, since the online softmax
-// does not care which rows it has seen.  It then writes one partial per query
-// head to slot j, counts the visit in each head's visit count and looks for
-// the next slab.  No CU idles while rows remain and faster CUs simply take more chunks.
-// Nothing here waits on another workgroup or needs a device-wide fence: the
-// merge, a separate launch, sees every partial.
+// A slab is the cache rows of one (b, KV head, head group).  A fixed set of
+// workgroups (one per CU and wave slot) stays resident.  Each first works
+// through its static range (see "Static part of the schedule" above): one
+// "visit" per slab the range meets.  Its last static visit (the home visit)
+// then goes on with the dynamic units of the same slab, taken one at a time
+// from the slab's counter.  When those run out the workgroup opens dynamic
+// visits on other slabs with units left, taking in one atomic step a slot
+// after the slab's static ones and the first two units, so every dynamic
+// visit has rows and the slots in use are exactly 0 .. visits-1.  A visit
+// folds all its rows -- its four waves interleave each segment's 16-row
+// tiles, so the workgroup streams one contiguous run of K and of V -- into
+// one running (max, sum, weighted sum) state, since the online softmax does
+// not care which rows it has seen, then writes one partial per query head to
+// its slot and counts the visit in each head's visit count.  Faster CUs
+// simply take more units at the end.  Nothing here waits on another
+// workgroup or needs a device-wide fence: the merge, a separate launch, sees
+// every partial.
 //
-//   slab line  per slab one 128-byte line: a 64-bit word {chunks taken (low),
-//              visits opened (high)}; reset by the merge
+//   slab line  per slab one 128-byte line: a 64-bit word {dynamic units
+//              taken (low), dynamic visits opened (high)}; reset by the merge
 //   nvis       [B][h_q] uint32 visits per query head; reset by the merge
 //   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum)
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
@@ -533,8 +540,8 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
   const int i = lane & 15;
   const int k = lane >> 4;
 
-  __shared__ int sh_ctl[7];      // slab, slot, first static chunk, static chunks, d0, d1, dynamic
-  __shared__ int sh_next[2];     // dynamic chunk after next, by parity
+  __shared__ int sh_ctl[7];      // slab, slot, static rows [sr, er), units d0 d1, dynamic
+  __shared__ int sh_next[2];     // dynamic unit after next, by parity
   __shared__ f4 sh_q[NB][DK / 16][kWave];
   __shared__ f4 sh_acc[kWaves - 1][NB][DV / 64][4][kWave];
   __shared__ float sh_m[kWaves - 1][NB][kWave];
@@ -592,10 +599,10 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
   while (true) {
     // ---- wave 0 opens a visit.  First the static visits of this
     // workgroup's range, one per slab the range meets; the last of them (the
-    // home visit) goes on with the dynamic chunks of its slab.  Then dynamic
-    // visits on any slab with dynamic chunks and slots left: lane 0 takes the
-    // slot and the first two chunks with one compare-and-swap on the slab's
-    // {chunks, visits} word, so every such visit has at least one chunk and
+    // home visit) goes on with the dynamic units of its slab.  Then dynamic
+    // visits on any slab with dynamic units and slots left: lane 0 takes the
+    // slot and the first two units with one compare-and-swap on the slab's
+    // {units, visits} word, so every such visit has at least one unit and
     // no slab gets more than Jd of them.
     if (wave == 0) {
       int s = -1, j = -1, sr = 0, er = 0, d0 = -1, d1 = -1, dyn = 0;
@@ -666,7 +673,7 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
           }
         }
         got = __shfl(got, 0);
-        if (got == ~0ull) continue;                     // no chunk or slot left meanwhile
+        if (got == ~0ull) continue;                     // no unit or slot left meanwhile
         s = cand;
         d0 = (int)(unsigned)got;
         d1 = d0 + 1;
@@ -854,7 +861,7 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
           }
           t += R;
           // A wave whose remaining tiles all lie past the slab's end (only
-          // in the slab's last chunk) leaves early instead of idling through
+          // in the slab's last segment) leaves early instead of idling through
           // them.
         } while (t < ctpw && row_of(t) <= last_row);
         if (tid == 0 && req) sh_next[it & 1] = after;
@@ -1056,8 +1063,8 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
 // Host side: validation, sizing, launches.
 // ---------------------------------------------------------------------------
 struct Plan {
-  int chunk_rows;     // rows per static chunk
-  int dyn_rows;       // rows per dynamic chunk (one ring turn of the 4 waves)
+  int chunk_rows;     // most rows per segment
+  int dyn_rows;       // rows per scheduling unit (one ring turn of the 4 waves)
   int fnum;           // static share of the rows, in sixteenths (0: all dynamic)
   int head_groups;    // groups of up to 32 query heads per KV head
   int blocks;         // MFMA column blocks per wave (1 or 2)
@@ -1118,7 +1125,7 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   plan->dyn_rows = plan->fnum > 0 ? ring * kWaves * kTileRows : chunk_rows;
   // Static slots: at most one per static unit of a slab plus one, and never
   // more than the workgroups.  Dynamic slots: every dynamic visit holds at
-  // least one chunk; kVisitSlack times the even share of workgroups per slab
+  // least one unit; kVisitSlack times the even share of workgroups per slab
   // leaves room for workgroups that move on from finished slabs.
   const int64_t Js =
       plan->fnum > 0 ? std::min<int64_t>(plan->grid, ceil_div(n_max, plan->dyn_rows)) + 1 : 0;
