@@ -229,6 +229,40 @@ def test_thousands_of_slabs_ragged(cuda_device):
     check(got, ref, "2400 slabs")
 
 
+SCHEDULE = [
+    # name, B, h_q, h_kv, d_k, d_v, n_max, lens
+    # fewer static units than workgroups: most ranges are empty, most rows
+    # dynamic, several sequences without any static unit
+    ("sparse_static", 8, 8, 1, 64, 64, 8192, [10, 20, 30, 5, 0, 1, 200, 1000]),
+    # every workgroup's static range spans several slabs
+    ("ranges_span_slabs", 64, 16, 8, 64, 64, 800, "ragged"),
+    # more sequences than the static part handles: dynamic units of whole
+    # segments only, on multi-segment slabs
+    ("many_sequences_dynamic", 300, 4, 2, 64, 64, 1000, "ragged"),
+    # two column blocks: the full resident grid of two workgroups per CU
+    # (interleaved ranks) on a ragged batch
+    ("two_blocks_ragged", 8, 64, 2, 64, 64, 16384, "ragged"),
+]
+
+
+@pytest.mark.parametrize("case", SCHEDULE, ids=[c[0] for c in SCHEDULE])
+def test_schedule_edge_cases(cuda_device, case):
+    """Static ranges and dynamic units cover every row exactly once however
+    the lengths fall: compared with the oracle, with NaN-poisoned partial
+    slots (a slot never written would show)."""
+    name, B, h_q, h_kv, d_k, d_v, n_max, lens = case
+    if lens == "ragged":
+        lens = np.random.default_rng(zlib.crc32(name.encode())).integers(0, n_max + 1, size=B)
+        lens[:2] = [0, n_max]
+    lens = np.asarray(lens, dtype=np.int32)
+    shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v, n_max=n_max)
+    inp = workloads.make(shape, seed=21, lens=lens)
+    say(f"schedule {name}: decode")
+    got = run_decode(inp, cuda_device)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, name)
+
+
 def test_two_million_rows_one_slab(cuda_device):
     """One sequence of 2^21 + 5 rows (a slab of 512 MiB per tensor at d=64):
     row offsets beyond 2^31 bytes."""
