@@ -21,7 +21,10 @@ Prints ONE JSON line:
                HIP events on the stream it runs on, against the 8 TB/s HBM peak;
                `traffic` = HBM bytes per launch from rocprofv3 FETCH_SIZE and
                WRITE_SIZE counters (profiles/decode_partial_counters.json),
-               null when the kernel source changed since they were taken.
+               null when the kernel source changed since they were taken;
+               `ceiling` = a plain streaming read of the same K and V
+               allocations on this machine (the practical read ceiling) and
+               the partial kernel's bandwidth as a fraction of it.
   cpu_baseline the CPU oracle (plain fp64 loops, OpenMP over heads) timed on
                this host on a bounded sample of the same workload.
 
@@ -74,6 +77,27 @@ def counter_traffic(workload: str):
     if c.get("kernel_build_sha256") != kernel_build_hash() or c.get("workload") != workload:
         return None
     return c.get("hbm_bytes_per_launch")
+
+
+def read_ceiling(a, b, stream, reps: int = 5):
+    """Mean GB/s of a plain streaming read of device tensors a and b (the
+    practical HBM read ceiling on those buffers), and the bytes read."""
+    import torch
+
+    from paper_2607_19456_amd import hbm_probe
+
+    nbytes = a.numel() * a.element_size() + b.numel() * b.element_size()
+    partial = hbm_probe.read(a, b, stream=stream)
+    ms = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        hbm_probe.read(a, b, partial=partial, stream=stream)
+        e1.record(stream)
+        e1.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    return nbytes / (sum(ms) / len(ms) * 1e-3) / 1e9, nbytes
 
 
 def host_cores() -> int:
@@ -459,6 +483,19 @@ def main() -> int:
     }
     log(f"{ms_per_step * 1e3:.1f} us/step, {value:.0f} GB/s; partial "
         f"{launch_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
+
+    # The machine's practical read ceiling on the same K and V allocations:
+    # a plain non-temporal streaming read of every byte (not the decode).
+    ceil_gbps, ceil_bytes = read_ceiling(dK, dV, stream)
+    result["roofline"]["ceiling"] = {
+        "achieved": round(ceil_gbps, 2), "unit": "GB/s", "bytes": ceil_bytes,
+        "kind": "streaming read of the same K and V allocations (hbm_probe: 16-byte "
+                "non-temporal loads, 8 in flight per thread, one workgroup per CU), "
+                "mean of 5 after 1 warm-up",
+        "frac": round(achieved / ceil_gbps, 4),
+    }
+    log(f"read ceiling on the same buffers: {ceil_gbps:.0f} GB/s; the decode's partial "
+        f"kernel reaches {achieved / ceil_gbps:.1%} of it")
 
     first_out = None
     if args.cpu_seconds > 0:

@@ -14,6 +14,10 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "decode_attn.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdecode_attn.so")
+# The read-ceiling probe the benchmark reports beside the decode (not part of
+# the decode).
+PROBE_SRC = os.path.join(PKG, "csrc", "hbm_probe.hip")
+PROBE_LIB = os.path.join(PKG, "libhbm_probe.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -35,15 +39,21 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile the library (always; a stale build must never be used)."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, "-o", tmp, SRC]
+def _compile(src: str, lib: str, verbose: bool) -> str:
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, *FLAGS, "-o", tmp, src]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the decode library and the read-ceiling probe (always; a stale
+    build must never be used).  Returns the decode library's path."""
+    _compile(PROBE_SRC, PROBE_LIB, verbose)
+    return _compile(SRC, LIB, verbose)
 
 
 if __name__ == "__main__":

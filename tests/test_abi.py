@@ -219,3 +219,16 @@ def test_product_path_does_not_reference_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "liboracle" not in text, f
+
+
+def test_read_probe_library_loads_and_validates():
+    """The read-ceiling probe the benchmark uses: its library loads, and bad
+    arguments are rejected on the host (no launch)."""
+    from paper_2607_19456_amd import hbm_probe
+    p = hbm_probe._lib
+    assert p.hbm_probe_threads() == 256
+    assert p.hbm_read_probe(FAKE, 16, FAKE, 16, None, 1, None) == 1      # no output
+    assert p.hbm_read_probe(None, 16, FAKE, 16, FAKE, 1, None) == 1      # NULL input
+    assert p.hbm_read_probe(FAKE + 4, 16, FAKE, 16, FAKE, 1, None) == 1  # misaligned
+    assert p.hbm_read_probe(FAKE, 20, FAKE, 16, FAKE, 1, None) == 2      # size not 16k
+    assert p.hbm_read_probe(FAKE, 16, FAKE, 16, FAKE, 0, None) == 2      # no workgroups
