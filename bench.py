@@ -79,6 +79,24 @@ def counter_traffic(workload: str):
     return c.get("hbm_bytes_per_launch")
 
 
+def custom_shape(spec: str):
+    """A workload from 'key=value,...' (keys of workloads.custom)."""
+    from paper_2607_19456_amd import workloads
+
+    kw = {}
+    for item in spec.split(","):
+        key, _, val = item.partition("=")
+        kw[key.strip()] = int(val)
+    steps, rows = kw.get("steps", 0), kw.get("rows", 1)
+    if "len_lo" not in kw:
+        kw["len_lo"] = max(1, kw["n_max"] - steps * rows)
+    kw.setdefault("len_hi", kw["len_lo"])
+    name = ("custom_B{B}_hq{h_q}_hkv{h_kv}_dk{d_k}_dv{d_v}_n{n_max}_len{len_lo}-{len_hi}"
+            .format(**kw) + (f"_{steps}steps" if steps else "") +
+            (f"_x{rows}rows" if rows > 1 else ""))
+    return workloads.custom(name, **kw)
+
+
 def read_ceiling(a, b, stream, reps: int = 5):
     """Mean GB/s of a plain streaming read of device tensors a and b (the
     practical HBM read ceiling on those buffers), and the bytes read."""
@@ -253,6 +271,11 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5")
+    ap.add_argument("--shape", default="",
+                    help="a custom workload instead of --workload, e.g. "
+                         "'B=8,h_q=32,h_kv=8,d_k=64,d_v=64,n_max=32768,steps=8' "
+                         "(also len_lo, len_hi, rows; lengths default to n_max, less "
+                         "steps*rows when there are steps)")
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle sample (0: skip)")
@@ -289,7 +312,7 @@ def main() -> int:
         print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
         return 0
 
-    shape = workloads.get(args.workload)
+    shape = custom_shape(args.shape) if args.shape else workloads.get(args.workload)
     s = shape
     log(f"workload {s.name}: drawing inputs")
     t0 = time.perf_counter()

@@ -89,9 +89,11 @@ constexpr int kVisitSlack = 4;
 // Static share of each slab's rows, in sixteenths: the first
 // floor(14/16 * rows / Cd) units of Cd rows (one turn of the tile ring) of
 // every slab are divided among the workgroups in advance, the rest is handed
-// out dynamically one unit at a time.  Batches of more than kMaxStaticSeqs
-// sequences would make the per-workgroup prefix sums long: they are
-// scheduled dynamically only.
+// out dynamically one unit at a time.  With at least two slabs per resident
+// workgroup (one column block) the share is 16/16: every slab is wholly
+// static, ceil(rows / Cd) units, and nothing is searched for or claimed.
+// Batches of more than kMaxStaticSeqs sequences would make the
+// per-workgroup prefix sums long: they are scheduled dynamically only.
 constexpr int kStaticDen = 16;
 constexpr int kStaticNum = 14;
 constexpr int kMaxStaticSeqs = 256;
@@ -362,7 +364,8 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
 //
 // Rows are scheduled in units of Cd rows (one turn of the tile ring for all
 // four waves).  Every slab of sequence b holds st(b) = floor(fnum/16 * n_b /
-// Cd) static units at its start; the rest of its rows is its dynamic part,
+// Cd) static units at its start (ceil(n_b / Cd), all of it, for fnum = 16);
+// the rest of its rows is its dynamic part,
 // handed out one unit at a time.  The static units of all slabs, in slab
 // order, form one space of Ru units that is cut into gridDim.x contiguous
 // ranges, [w*Ru/G, (w+1)*Ru/G) for workgroup w: the ranges are proportional
@@ -371,6 +374,7 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
 // slabs; each (workgroup, slab) pair is a visit with its own partial slot.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int static_units(int n_b, int Cd, int fnum) {
+  if (fnum >= kStaticDen) return (n_b + Cd - 1) / Cd;          // the whole slab
   return (int)((int64_t)n_b * fnum / ((int64_t)kStaticDen * Cd));
 }
 
@@ -529,6 +533,8 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
     int B, int h_q, int h_kv, int n_max, int T, int C, int Cd, int fnum, int head_groups, int J,
     int Jd, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
     float* __restrict__ ws_acc, float* __restrict__ out_direct) {
+  // Whole-slab static ranges are planned for one column block only.
+  if (NB == 2 && fnum > kStaticNum) fnum = kStaticNum;
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
@@ -588,6 +594,7 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
                        ? (int)(blockIdx.x % kComputeUnits) * 2 + (int)(blockIdx.x / kComputeUnits)
                        : (int)blockIdx.x;
   int64_t Ru = 0, u_lo = 0, u_hi = 0;
+  int ws_s = -1, ws_st = 0;         // slab and units per slab of the last static visit
   if (wave == 0 && fnum > 0) {
     int64_t before;
     int st;
@@ -606,7 +613,7 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
     // no slab gets more than Jd of them.
     if (wave == 0) {
       int s = -1, j = -1, sr = 0, er = 0, d0 = -1, d1 = -1, dyn = 0;
-      int budget = out_direct ? 0 : S;
+      int budget = (out_direct || fnum >= kStaticDen) ? 0 : S;
       if (out_direct) {
         if (first) {
           s = blockIdx.x;
@@ -614,21 +621,34 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
           er = C;
         }
       } else if (u_lo < u_hi) {
+        // The slab holding unit u_lo.  A static visit that is not the last
+        // of its range ends at its slab's end, so with whole-slab ranges the
+        // next visit is the next slab of the same sequence (same units) if
+        // there is one; otherwise a search over the sequences' prefix sums.
         int64_t fu = 0;
-        int stb = 0;
-        const int bs =
-            static_locate(len, B, n_max, app, T, Cd, fnum, per_b, u_lo, lane, &fu, &stb);
+        int stb = 0, bs, r;
+        int64_t Ps;
+        if (fnum >= kStaticDen && ws_s >= 0 && (ws_s + 1) % per_b != 0) {
+          bs = (ws_s + 1) / per_b;
+          r = (ws_s + 1) % per_b;
+          stb = ws_st;
+          Ps = u_lo;
+        } else {
+          bs = static_locate(len, B, n_max, app, T, Cd, fnum, per_b, u_lo, lane, &fu, &stb);
+          r = stb > 0 ? (int)((u_lo - fu) / stb) : 0;
+          Ps = fu + (int64_t)r * stb;
+        }
         if (bs >= 0 && stb > 0) {
-          const int r = (int)((u_lo - fu) / stb);
-          const int64_t Ps = fu + (int64_t)r * stb;
           const int64_t e = u_hi < Ps + stb ? u_hi : Ps + stb;
           s = bs * per_b + r;
           j = static_slot(Ps, u_lo, Ru, Gw, rank);
           sr = (int)(u_lo - Ps) * Cd;
           er = (int)(e - Ps) * Cd;
           u_lo = e;
+          ws_s = s;
+          ws_st = stb;
           budget = 0;
-          if (u_lo == u_hi) {
+          if (u_lo == u_hi && fnum < kStaticDen) {
             // The home visit.  If its static rows do not fill the
             // two-segment window, its first dynamic units are taken now.
             dyn = 1;
@@ -1117,8 +1137,15 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
       (int64_t)kComputeUnits * (plan->blocks == 2 && d_k + d_v <= 256 ? 2 : 1);
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
   // Static share: off for single-chunk caches (direct form) and for batches
-  // whose per-workgroup prefix over sequences would be long.
-  plan->fnum = (!plan->single_chunk && B <= kMaxStaticSeqs) ? kStaticNum : 0;
+  // whose per-workgroup prefix over sequences would be long.  With two or
+  // more slabs per workgroup the even split of whole slabs balances the
+  // grid by itself and the dynamic searches over many slabs are saved
+  // (one column block only: the two-block kernel is register-bound and
+  // keeps the 14/16 share).
+  plan->fnum = 0;
+  if (!plan->single_chunk && B <= kMaxStaticSeqs)
+    plan->fnum = plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid
+                      ? kStaticDen : kStaticNum;
   // Scheduling units (static ranges and dynamic hand-outs) are one ring turn
   // of the four waves when there is a static share, else whole chunks.
   const int ring = (plan->blocks == 2 || d_k + d_v > 256) ? 2 : 3;

@@ -234,11 +234,18 @@ SCHEDULE = [
     # fewer static units than workgroups: most ranges are empty, most rows
     # dynamic, several sequences without any static unit
     ("sparse_static", 8, 8, 1, 64, 64, 8192, [10, 20, 30, 5, 0, 1, 200, 1000]),
-    # every workgroup's static range spans several slabs
+    # two or more slabs per workgroup (one column block): every slab wholly
+    # static, no dynamic units; a range walks from slab to slab, within a
+    # sequence and across sequences
     ("ranges_span_slabs", 64, 16, 8, 64, 64, 800, "ragged"),
+    # the same with 128 slabs per sequence
+    ("wide_sequences_all_static", 4, 128, 128, 64, 64, 1000, "ragged"),
     # more sequences than the static part handles: dynamic units of whole
     # segments only, on multi-segment slabs
     ("many_sequences_dynamic", 300, 4, 2, 64, 64, 1000, "ragged"),
+    # two column blocks with many slabs per workgroup keep the 14/16 static
+    # share with dynamic remainders
+    ("two_blocks_many_slabs", 128, 256, 8, 64, 64, 800, "ragged"),
     # two column blocks: the full resident grid of two workgroups per CU
     # (interleaved ranks) on a ragged batch
     ("two_blocks_ragged", 8, 64, 2, 64, 64, 16384, "ragged"),

@@ -73,3 +73,29 @@ def test_one_slab_holding_everything_uses_every_workgroup():
     # the worst case the static slot count is sized for: one slab, G slots
     P, Ru, visits = visits_and_slots([10_000], 256)
     assert sorted(v[3] for v in visits) == list(range(256))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_range_walks_slab_to_slab(seed):
+    """Whole-slab ranges: a visit that is not the last of its workgroup's
+    range ends at its slab's end, and the next visit starts at the first unit
+    of the next slab that has units, so the kernel can step to it without a
+    search (every slab of one sequence holds the same number of units)."""
+    rng = random.Random(100 + seed)
+    for _ in range(200):
+        per_b = rng.choice([1, 2, 8, 32])
+        B = rng.randint(1, 12)
+        G = rng.choice([1, 3, 64, 256])
+        seq_units = [rng.choice([0, 1, 2, 5, rng.randint(0, 40)]) for _ in range(B)]
+        units = [u for u in seq_units for _ in range(per_b)]
+        if sum(units) == 0:
+            continue
+        P, Ru, visits = visits_and_slots(units, G)
+        for (w0, s0, r0, _), (w1, s1, r1, _) in zip(visits, visits[1:]):
+            if w0 != w1:
+                continue
+            assert r0.stop == P[s0] + units[s0]
+            assert s1 == next(i for i in range(s0 + 1, len(units)) if units[i] > 0)
+            assert r1.start == P[s1]
+            if (s0 + 1) % per_b != 0:
+                assert s1 == s0 + 1 and units[s1] == units[s0]
