@@ -56,7 +56,7 @@ typedef enum da_status {
     DA_OK = 0,
     DA_ERR_NULL = 1,        /* a required pointer is NULL                          */
     DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q,
-                               or chunk_rows not a positive multiple of 384        */
+                               or chunk_rows not a positive multiple of 768        */
     DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128, 256} (decode), or not a
                                multiple of 4 (append)                              */
     DA_ERR_ALIGN = 4,       /* a float array not 16-byte aligned, len not 4-byte   */
@@ -84,7 +84,7 @@ const char *da_status_string(int status);
 
 /*
  * Rows per work segment the library picks for these shapes when chunk_rows
- * is 0 below (a positive multiple of 384).  Returns 0 if the shapes are
+ * is 0 below (a positive multiple of 768).  Returns 0 if the shapes are
  * invalid.
  */
 int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);

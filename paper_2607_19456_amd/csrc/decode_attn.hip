@@ -59,30 +59,26 @@ constexpr int kHeadsPerBlock = 16;                   // heads per MFMA column bl
 constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgroup
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
 constexpr int kComputeUnits = 256;                   // MI355X
-// Register tiles per wave in the load ring, and waves per SIMD, of the
-// partial kernel.  One column block (<= 16 query rows per KV head): a
-// three-tile ring at one wave per SIMD keeps two tiles' loads in flight
-// during each tile's products (two tiles at two waves per SIMD measured the
-// same on long contexts and 2-3 % slower on the shorter ones).  Two column
-// blocks double the matrix work per tile: there a two-tile ring at two waves
-// per SIMD, whose registers fit without parking the accumulators in AGPRs and
-// whose second wave overlaps one wave's softmax with the other's products,
-// is 5 % (MQA) to 10 % (four query rows per head) faster.
-// A tile of d_k = d_v = 256 holds 128 registers per lane: such head sizes
-// take a two-tile ring at one wave per SIMD.
+// Register tiles per wave in the load ring of the partial kernel, which
+// runs one wave per SIMD (all 512 registers of a lane).  One column block
+// (<= 16 query rows per KV head): a three-tile ring keeps two tiles' loads in
+// flight during each tile's products (two tiles at two waves per SIMD
+// measured the same on long contexts and 2-3 % slower on the shorter ones).
+// Two column blocks double the matrix work per tile: a four-tile ring (three
+// tiles in flight), with both blocks' score chains, softmax updates and
+// weighted sums issued side by side, is 6 % faster on MQA than a two-tile
+// ring at two waves per SIMD, 7 % faster than a three-tile ring.  A tile of
+// d_k = d_v = 256 holds 128 registers per lane: such head sizes take a
+// two-tile ring.
 template <int NB, int DK, int DV>
-constexpr int kRing = (NB == 2 || DK + DV > 256) ? 2 : 3;
-template <int NB, int DK, int DV>
-constexpr int kWavesPerSimd = (NB == 2 && DK + DV <= 256) ? 2 : 1;
+constexpr int kRing = DK + DV > 256 ? 2 : (NB == 2 ? 4 : 3);
 // A segment (chunk_rows) is the most rows a workgroup reads in one go from
-// its static range, a multiple of six 16-row tiles per wave (whole turns of
-// either ring); with no static share (single-chunk caches, very large
-// batches) it is also the unit handed out dynamically.  The default is 768
-// rows for one column block and 384 for two (measured).
-constexpr int kChunkQuantum = 6 * kTileRows * kWaves;
-static_assert(6 % 2 == 0 && 6 % 3 == 0, "chunks are whole turns of either ring");
+// its static range, a multiple of twelve 16-row tiles per wave (whole turns
+// of every ring); with no static share (single-chunk caches, very large
+// batches) it is also the unit handed out dynamically.
+constexpr int kChunkQuantum = 12 * kTileRows * kWaves;
+static_assert(12 % 2 == 0 && 12 % 3 == 0 && 12 % 4 == 0, "chunks are whole turns of every ring");
 constexpr int kDefaultChunkRows = 768;
-constexpr int kDefaultChunkRows2 = 384;
 // Visit slots per slab for dynamic visits, in units of the even share of
 // resident workgroups per slab.
 constexpr int kVisitSlack = 4;
@@ -293,10 +289,80 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
                                              const f4 (*__restrict__ sh_q)[DK / 16][kWave],
                                              float (&m_run)[NB], float (&l_run)[NB],
                                              f4 (&acc)[NB][DV / 64][4]) {
-  // q is re-read from LDS for every tile rather than pinned in 32 VGPRs per
-  // column block: the empty asm keeps the compiler from hoisting those reads
-  // out of the tile loop, which would cost a second wave per SIMD.
+  // q is re-read from LDS for every tile rather than pinned in 32 registers
+  // per column block, which are left to the load ring: the empty asm keeps
+  // the compiler from hoisting those reads out of the tile loop.
   asm volatile("" ::: "memory");
+  if constexpr (NB == 2) {
+    // Both column blocks in step: their score chains (four independent
+    // accumulators sharing each K operand), then both softmax updates, then
+    // both weighted sums sharing each V operand.
+    f4 sa0 = f4{0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
+#pragma unroll
+    for (int t = 0; t < DK / 16; t += 2) {
+      const f4 qa0 = sh_q[0][t][lane], qa1 = sh_q[0][t + 1][lane];
+      const f4 qb0 = sh_q[1][t][lane], qb1 = sh_q[1][t + 1][lane];
+      sa0 = mfma_16x16x4(T.k[t].x, qa0.x, sa0);
+      sb0 = mfma_16x16x4(T.k[t].x, qb0.x, sb0);
+      sa1 = mfma_16x16x4(T.k[t + 1].x, qa1.x, sa1);
+      sb1 = mfma_16x16x4(T.k[t + 1].x, qb1.x, sb1);
+      sa0 = mfma_16x16x4(T.k[t].y, qa0.y, sa0);
+      sb0 = mfma_16x16x4(T.k[t].y, qb0.y, sb0);
+      sa1 = mfma_16x16x4(T.k[t + 1].y, qa1.y, sa1);
+      sb1 = mfma_16x16x4(T.k[t + 1].y, qb1.y, sb1);
+      sa0 = mfma_16x16x4(T.k[t].z, qa0.z, sa0);
+      sb0 = mfma_16x16x4(T.k[t].z, qb0.z, sb0);
+      sa1 = mfma_16x16x4(T.k[t + 1].z, qa1.z, sa1);
+      sb1 = mfma_16x16x4(T.k[t + 1].z, qb1.z, sb1);
+      sa0 = mfma_16x16x4(T.k[t].w, qa0.w, sa0);
+      sb0 = mfma_16x16x4(T.k[t].w, qb0.w, sb0);
+      sa1 = mfma_16x16x4(T.k[t + 1].w, qa1.w, sa1);
+      sb1 = mfma_16x16x4(T.k[t + 1].w, qb1.w, sb1);
+    }
+    f4 sc[2] = {sa0 + sa1, sb0 + sb1};
+    f4 pr[2];
+    float alpha[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (row0 + 4 * k + r > lim[nb]) sc[nb][r] = -INFINITY;
+      const float tmax =
+          max_over_row_groups(fmaxf(fmaxf(sc[nb][0], sc[nb][1]), fmaxf(sc[nb][2], sc[nb][3])));
+      const float m_new = fmaxf(m_run[nb], tmax);
+      float m_ref = m_new;
+      if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
+      alpha[nb] = fast_exp2(m_run[nb] - m_ref);
+      pr[nb][0] = fast_exp2(sc[nb][0] - m_ref);
+      pr[nb][1] = fast_exp2(sc[nb][1] - m_ref);
+      pr[nb][2] = fast_exp2(sc[nb][2] - m_ref);
+      pr[nb][3] = fast_exp2(sc[nb][3] - m_ref);
+      l_run[nb] = l_run[nb] * alpha[nb] + ((pr[nb][0] + pr[nb][1]) + (pr[nb][2] + pr[nb][3]));
+      m_run[nb] = m_new;
+    }
+    if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int c = 0; c < DV / 64; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha[nb];
+    }
+#pragma unroll
+    for (int rho = 0; rho < 4; ++rho)
+#pragma unroll
+      for (int c = 0; c < DV / 64; ++c) {
+        acc[0][c][0] = mfma_16x16x4(T.v[rho][c].x, pr[0][rho], acc[0][c][0]);
+        acc[1][c][0] = mfma_16x16x4(T.v[rho][c].x, pr[1][rho], acc[1][c][0]);
+        acc[0][c][1] = mfma_16x16x4(T.v[rho][c].y, pr[0][rho], acc[0][c][1]);
+        acc[1][c][1] = mfma_16x16x4(T.v[rho][c].y, pr[1][rho], acc[1][c][1]);
+        acc[0][c][2] = mfma_16x16x4(T.v[rho][c].z, pr[0][rho], acc[0][c][2]);
+        acc[1][c][2] = mfma_16x16x4(T.v[rho][c].z, pr[1][rho], acc[1][c][2]);
+        acc[0][c][3] = mfma_16x16x4(T.v[rho][c].w, pr[0][rho], acc[0][c][3]);
+        acc[1][c][3] = mfma_16x16x4(T.v[rho][c].w, pr[1][rho], acc[1][c][3]);
+      }
+    return;
+  }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     f4 qb[DK / 16];
@@ -526,7 +592,7 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_partial_kernel(
+__global__ __launch_bounds__(kThreads, 1) void decode_partial_kernel(
     const float* __restrict__ q, float* __restrict__ K,
     float* __restrict__ V, const float* __restrict__ k_new,
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
@@ -584,15 +650,8 @@ __global__ __launch_bounds__(kThreads, (kWavesPerSimd<NB, DK, DV>)) void decode_
   // rows itself -- no merge, and no other workgroup touches its counter line.
   bool first = true;
   // This workgroup's static range, units [u_lo, u_hi) of Ru (wave 0 only).
-  // Ranges go by rank.  With two resident workgroups per CU (two waves per
-  // SIMD) workgroups w and w + 256 share a CU, and the older one's waves win
-  // the issue arbitration, so it runs markedly faster: ranking them next to
-  // each other puts both kinds on every slab, where the faster ones drain
-  // the slab's dynamic part.
   const int Gw = (int)gridDim.x;
-  const int rank = Gw == 2 * kComputeUnits
-                       ? (int)(blockIdx.x % kComputeUnits) * 2 + (int)(blockIdx.x / kComputeUnits)
-                       : (int)blockIdx.x;
+  const int rank = (int)blockIdx.x;
   int64_t Ru = 0, u_lo = 0, u_hi = 0;
   int ws_s = -1, ws_st = 0;         // slab and units per slab of the last static visit
   if (wave == 0 && fnum > 0) {
@@ -1118,7 +1177,7 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int G = h_q / h_kv;
   if (chunk_rows == 0) {
     // The default, or the whole cache rounded up to the quantum if shorter.
-    chunk_rows = G > kHeadsPerBlock ? kDefaultChunkRows2 : kDefaultChunkRows;
+    chunk_rows = kDefaultChunkRows;
     chunk_rows = (int)std::min<int64_t>(chunk_rows,
                                         ceil_div(n_max, kChunkQuantum) * kChunkQuantum);
   }
@@ -1130,25 +1189,21 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   plan->merge_heads = std::min(G, plan->blocks * kHeadsPerBlock);
   const int64_t chunks_per_slab = ceil_div(n_max, chunk_rows);
   plan->single_chunk = chunks_per_slab == 1;
-  // One resident workgroup per CU and wave slot, fewer if there are fewer
-  // chunks than that.
-  // (two waves per SIMD only for two column blocks at d_k + d_v <= 256)
-  const int64_t resident =
-      (int64_t)kComputeUnits * (plan->blocks == 2 && d_k + d_v <= 256 ? 2 : 1);
+  // One resident workgroup per CU, fewer if there are fewer chunks than that.
+  const int64_t resident = kComputeUnits;
   plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
   // Static share: off for single-chunk caches (direct form) and for batches
   // whose per-workgroup prefix over sequences would be long.  With two or
   // more slabs per workgroup the even split of whole slabs balances the
   // grid by itself and the dynamic searches over many slabs are saved
-  // (one column block only: the two-block kernel is register-bound and
-  // keeps the 14/16 share).
+  // (one column block only: with two, whole slabs measured 0-1.5 % slower).
   plan->fnum = 0;
   if (!plan->single_chunk && B <= kMaxStaticSeqs)
     plan->fnum = plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid
                       ? kStaticDen : kStaticNum;
   // Scheduling units (static ranges and dynamic hand-outs) are one ring turn
   // of the four waves when there is a static share, else whole chunks.
-  const int ring = (plan->blocks == 2 || d_k + d_v > 256) ? 2 : 3;
+  const int ring = d_k + d_v > 256 ? 2 : (plan->blocks == 2 ? 4 : 3);
   plan->dyn_rows = plan->fnum > 0 ? ring * kWaves * kTileRows : chunk_rows;
   // Static slots: at most one per static unit of a slab plus one, and never
   // more than the workgroups.  Dynamic slots: every dynamic visit holds at

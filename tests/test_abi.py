@@ -44,8 +44,8 @@ def test_status_strings():
 
 def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     """The sizing rule, restated: rows are scheduled in units of one ring
-    turn (64 rows per tile of the ring: 3 tiles, or 2 for two column blocks
-    or large heads); per (b, query head) one visit slot for each static
+    turn (64 rows per tile of the ring: 3 tiles for one column block, 4 for
+    two, 2 for large heads); per (b, query head) one visit slot for each static
     visit a slab can have (at most one per unit plus one, and at most one per
     resident workgroup) and, for dynamic visits, up to 4x the even share of
     resident workgroups per slab (at most one per unit); one 128-byte
@@ -57,11 +57,10 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     groups = -(-G // 32)
     slabs = B * h_kv * groups
     chunks = -(-n_max // c)
-    # two waves per SIMD for two column blocks, unless the head sizes are large
-    resident = 256 * (2 if G > 16 and d_k + d_v <= 256 else 1)
+    resident = 256                      # one workgroup per CU
     grid = max(1, min(resident, chunks * slabs))
     static = chunks > 1 and B <= 256
-    ring = 2 if G > 16 or d_k + d_v > 256 else 3
+    ring = 2 if d_k + d_v > 256 else (4 if G > 16 else 3)
     dyn_rows = ring * 64 if static else c
     Js = min(grid, -(-n_max // dyn_rows)) + 1 if static else 0
     Jd = max(1, min(-(-n_max // dyn_rows), 4 * -(-grid // slabs)))
@@ -77,15 +76,15 @@ def test_chunk_rows_and_workspace_sizes():
                  (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128),
                  (2, 64, 2, 5000, 256, 256), (2, 16, 2, 900, 256, 64)]:
         c = binding.chunk_rows(*args)
-        default = 384 if args[1] // args[2] > 16 else 768
-        assert c == min(default, -(-args[3] // 384) * 384)
+        assert c == min(768, -(-args[3] // 768) * 768)
         counters, total = _expected_workspace(*args, c)
         assert binding.workspace_counter_bytes(*args) == counters
         assert binding.workspace_bytes(*args) == total
-        assert binding.workspace_bytes(*args, 384) == _expected_workspace(*args, 384)[1]
+        assert binding.workspace_bytes(*args, 1536) == _expected_workspace(*args, 1536)[1]
     assert binding.chunk_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
     assert binding.workspace_bytes(1, 1, 1, 10, 96, 64) == 0  # unsupported d_k
-    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 192) == 0  # chunk not a multiple of 384
+    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 192) == 0  # chunk not a multiple of 768
+    assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 384) == 0
 
 
 def _decode(**kw):
@@ -103,7 +102,7 @@ def _decode(**kw):
     (dict(out=None), 1),
     (dict(B=0), 2), (dict(h_q=0), 2), (dict(h_kv=0), 2), (dict(n_max=0), 2),
     (dict(h_q=3, h_kv=2), 2), (dict(B=1 << 21), 2), (dict(chunk=100), 2),
-    (dict(chunk=192), 2), (dict(chunk=-384), 2),
+    (dict(chunk=192), 2), (dict(chunk=384), 2), (dict(chunk=-768), 2),
     (dict(d_k=96), 3), (dict(d_v=32), 3), (dict(d_k=512), 3),
     (dict(q=FAKE + 4), 4), (dict(K=FAKE + 8), 4), (dict(out=FAKE + 4), 4),
     (dict(len=FAKE + 2), 4),

@@ -64,7 +64,7 @@ MULTI = [
 
 
 @pytest.mark.parametrize("case", MULTI, ids=[c[0] for c in MULTI])
-@pytest.mark.parametrize("chunk_rows", [0, 384])
+@pytest.mark.parametrize("chunk_rows", [0, 768])
 def test_decode_multi(cuda_device, case, chunk_rows):
     name, B, h_q, h_kv, d_k, d_v, n_max, T, lens = case
     shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v, n_max=n_max)

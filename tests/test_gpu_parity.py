@@ -87,7 +87,7 @@ SMALL = [
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
-@pytest.mark.parametrize("chunk_rows", [0, 384, 1152])
+@pytest.mark.parametrize("chunk_rows", [0, 768, 1536])
 def test_decode_small_shapes(cuda_device, case, chunk_rows):
     name, B, h_q, h_kv, d_k, d_v, n_max, lens = case
     shape = workloads.custom(name, B=B, h_q=h_q, h_kv=h_kv, d_k=d_k, d_v=d_v,
@@ -105,7 +105,7 @@ def test_decode_small_shapes(cuda_device, case, chunk_rows):
 def test_chunk_size_invariance(cuda_device):
     shape = workloads.custom("chunks", B=2, h_q=8, h_kv=2, d_k=128, d_v=128, n_max=4096)
     inp = workloads.make(shape, seed=5, lens=np.array([4096, 3000], np.int32))
-    outs = [run_decode(inp, cuda_device, chunk_rows=c) for c in (384, 1152, 4224, 0)]
+    outs = [run_decode(inp, cuda_device, chunk_rows=c) for c in (768, 1536, 4608, 0)]
     for o in outs[1:]:
         assert np.max(np.abs(o - outs[0])) <= 1e-6
 
@@ -183,7 +183,7 @@ def test_one_slab_many_visits(cuda_device, h_q, h_kv):
                              n_max=n)
     inp = workloads.make(shape, seed=12, lens=np.array([n - 5], np.int32))
     say(f"one slab h_q={h_q}: decode")
-    got = run_decode(inp, cuda_device, chunk_rows=384)
+    got = run_decode(inp, cuda_device, chunk_rows=768)
     ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
     check(got, ref, f"one slab h_q={h_q}")
 
