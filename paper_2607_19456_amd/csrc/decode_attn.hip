@@ -836,34 +836,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_partial_kernel(
       }
     }
 
-    // B operand of the score product, staged in LDS in register order: entry
-    // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
-    // base-2 units (zero for the padding heads of a partial column block).
-    for (int e = tid; e < NB * (DK / 16) * kWave; e += kThreads) {
-      const int ln = e % kWave;
-      const int t = (e / kWave) % (DK / 16);
-      const int nb = e / (kWave * (DK / 16));
-      const int hl = nb * kHeadsPerBlock + (ln & 15);
-      f4 v = f4{0.f, 0.f, 0.f, 0.f};
-      if (hl < h_count)
-        v = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4)) * qscale;
-      sh_q[nb][t][ln] = v;
-    }
-    __syncthreads();
-
-    // Running state per column block; lane (k, i) belongs to head i.
-    float m_run[NB], l_run[NB];
-    f4 acc[NB][DV / 64][4];   // acc[nb][c][e][r] = O[dim 64c+16k+4r+e][head i]
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      m_run[nb] = -INFINITY;
-      l_run[nb] = 0.f;
-#pragma unroll
-      for (int cc = 0; cc < DV / 64; ++cc)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[nb][cc][e] = f4{0.f, 0.f, 0.f, 0.f};
-    }
-
     // The visit's rows are a stream of segments: its static rows [sr, er)
     // in segments of up to C rows, then, for the home visit and dynamic
     // visits, the slab's dynamic units in the order its counter hands them
@@ -905,12 +877,53 @@ __global__ __launch_bounds__(kThreads, 1) void decode_partial_kernel(
       return x < ctpw ? cs + x * kRowsPerTurn + wave * kTileRows
                       : (ns >= 0 ? ns + (x - ctpw) * kRowsPerTurn + wave * kTileRows : last_row);
     };
-    constexpr int R = kRing<NB, DK, DV>;
-    if (cs >= 0) {
-      Tile<DK, DV, NB> ring[R];
+    // B operand of the score product, staged in LDS in register order: entry
+    // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
+    // base-2 units (zero for the padding heads of a partial column block).
+    // The q loads go out first and the ring's first tiles right after them,
+    // so the tiles are in flight while q is written to LDS.
+    constexpr int kQPerThread = NB * (DK / 16) * kWave / kThreads;
+    static_assert(kQPerThread * kThreads == NB * (DK / 16) * kWave, "q staging");
+    f4 qv[kQPerThread];
 #pragma unroll
-      for (int p = 0; p < R - 1; ++p)
-        load_tile<DK, DV, NB, CAUSAL>(ring[p], src, row_of(p), last_row, i, k);
+    for (int u = 0; u < kQPerThread; ++u) {
+      const int e = tid + u * kThreads;
+      const int ln = e % kWave;
+      const int t = (e / kWave) % (DK / 16);
+      const int nb = e / (kWave * (DK / 16));
+      const int hl = nb * kHeadsPerBlock + (ln & 15);
+      qv[u] = f4{0.f, 0.f, 0.f, 0.f};
+      if (hl < h_count)
+        qv[u] = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4));
+    }
+    constexpr int R = kRing<NB, DK, DV>;
+    Tile<DK, DV, NB> ring[R];
+    // (Unconditional, so that the wait for q counts only the q loads; a
+    // visit without rows, which the schedule never opens, would read row 0.)
+#pragma unroll
+    for (int p = 0; p < R - 1; ++p)
+      load_tile<DK, DV, NB, CAUSAL>(ring[p], src, cs >= 0 ? row_of(p) : 0, max(last_row, 0), i, k);
+#pragma unroll
+    for (int u = 0; u < kQPerThread; ++u) {
+      const int e = tid + u * kThreads;
+      sh_q[e / (kWave * (DK / 16))][(e / kWave) % (DK / 16)][e % kWave] = qv[u] * qscale;
+    }
+    __syncthreads();
+
+    // Running state per column block; lane (k, i) belongs to head i.
+    float m_run[NB], l_run[NB];
+    f4 acc[NB][DV / 64][4];   // acc[nb][c][e][r] = O[dim 64c+16k+4r+e][head i]
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      m_run[nb] = -INFINITY;
+      l_run[nb] = 0.f;
+#pragma unroll
+      for (int cc = 0; cc < DV / 64; ++cc)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[nb][cc][e] = f4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    if (cs >= 0) {
       for (int it = 0;; ++it) {
         // The segment after next comes from the counter once the static
         // rows are all in the window.  Its value is left undefined for the
