@@ -70,8 +70,9 @@ const char *da_status_string(int status);
 
 /*
  * Workspace.  The decode keeps, per (b, query head), a few partial results
- * (running maximum, running sum of exponentials, unnormalised weighted sum of
- * V rows) plus a few counters per (b, KV head) that schedule the work.  The
+ * (a reference score, at most 8 base-2 units below the largest score seen,
+ * the sum of exponentials against it, the unnormalised weighted sum of V
+ * rows) plus a few counters per (b, KV head) that schedule the work.  The
  * counter region -- the first da_decode_workspace_counter_bytes() bytes --
  * must be zero before the first decode that uses the workspace (an all-zero
  * workspace always qualifies); every completed decode leaves it zero again,
@@ -157,8 +158,8 @@ da_status da_decode_step(const float *q, float *K, float *V,
 /*
  * First half of da_decode_attn / da_decode_step: scores of all G query heads
  * of each group over the slab's rows (K and V rows read from HBM once per
- * (b, KV head)), their running maxima, sums of exponentials and unnormalised
- * weighted sums of V rows, written to the workspace as per-visit partials.
+ * (b, KV head)), their reference scores, sums of exponentials and
+ * unnormalised weighted sums of V rows, written to the workspace as per-visit partials.
  * k_new and v_new are both NULL (plain decode; K and V are only read) or both
  * set (the fused append of da_decode_step: row len[b] of every KV head is
  * taken from them and written into K / V).  Must be followed by
@@ -173,7 +174,7 @@ da_status da_decode_partial(const float *q, float *K, float *V,
 
 /*
  * Second half: combines the partials of every (b, query head) into
- * out[b,h,:] (running maximum, rescaled sums, one division) and resets the
+ * out[b,h,:] (largest reference, rescaled sums, one division) and resets the
  * workspace counters to zero.  chunk_rows and the shapes must be those of the
  * da_decode_partial call that filled the workspace.  len is NULL after a
  * plain decode; after a partial with a fused append it is that call's len,

@@ -26,8 +26,8 @@
 //   (v_mfma_f32_16x16x4_f32, fp32 in and out):
 //     scores  S[16 rows x 16 heads] = K_tile[16 x d_k] . Q^T[d_k x 16]
 //     update  O^T[d_v x 16 heads]  += V_tile^T[d_v x 16] . P[16 x 16 heads]
-//   with the online (running max / running sum) form of the softmax between
-//   them, so the score vector never leaves registers.  Up to 16 query heads
+//   with the online (running reference / running sum) form of the softmax
+//   between them, so the score vector never leaves registers.  Up to 16 query heads
 //   ride in one product's columns; groups of 17..32 heads use two column
 //   blocks over the same K/V registers, larger groups several head groups.
 //   Scores are kept in base-2 units: q is pre-multiplied by scale*log2(e) and
@@ -55,6 +55,13 @@ constexpr int kWave = 64;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
 constexpr int kTileRows = 16;                        // rows per MFMA tile
+// Online softmax: each head's reference (the value its weights are
+// exponentiated against, base-2 units) is raised only when a tile's maximum
+// exceeds it by more than this, so a weight is at most 2^kLazyMax and the
+// accumulators are rescaled only on such a jump (the result is the same
+// softmax for any reference; the merge combines partials by their
+// references).
+constexpr float kLazyMax = 8.f;
 constexpr int kHeadsPerBlock = 16;                   // heads per MFMA column block
 constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgroup
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
@@ -329,7 +336,7 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
         if (row0 + 4 * k + r > lim[nb]) sc[nb][r] = -INFINITY;
       const float tmax =
           max_over_row_groups(fmaxf(fmaxf(sc[nb][0], sc[nb][1]), fmaxf(sc[nb][2], sc[nb][3])));
-      const float m_new = fmaxf(m_run[nb], tmax);
+      const float m_new = tmax > m_run[nb] + kLazyMax ? tmax : m_run[nb];
       float m_ref = m_new;
       if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
       alpha[nb] = fast_exp2(m_run[nb] - m_ref);
@@ -388,9 +395,10 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
     for (int r = 0; r < 4; ++r)
       if (row0 + 4 * k + r > lim[nb]) s[r] = -INFINITY;
 
-    // Step II, online: running max over the 4 row groups of head i.
+    // Step II, online: the tile's max over the 4 row groups of head i, and
+    // the head's reference (raised only on a jump above kLazyMax).
     const float tmax = max_over_row_groups(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
-    const float m_new = fmaxf(m_run[nb], tmax);
+    const float m_new = tmax > m_run[nb] + kLazyMax ? tmax : m_run[nb];
     // A causal column may have seen no row yet (m_new = -inf): exponentiate
     // against 0 then, so every weight is 0 instead of NaN.
     float m_ref = m_new;
@@ -403,8 +411,8 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
     pr[3] = fast_exp2(s[3] - m_ref);
     l_run[nb] = l_run[nb] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
     m_run[nb] = m_new;
-    // Once the running maxima settle, most tiles leave them unchanged
-    // (alpha = 1 in every lane): skip the rescale of the accumulators then.
+    // Most tiles leave every reference unchanged (alpha = 1 in every lane):
+    // skip the rescale of the accumulators then.
     if (__any(alpha != 1.f)) {
 #pragma unroll
       for (int c = 0; c < DV / 64; ++c)
@@ -578,7 +586,7 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 // visit has rows and the slots in use are exactly 0 .. visits-1.  A visit
 // folds all its rows -- its four waves interleave each segment's 16-row
 // tiles, so the workgroup streams one contiguous run of K and of V -- into
-// one running (max, sum, weighted sum) state, since the online softmax does
+// one running (reference, sum, weighted sum) state, since the online softmax does
 // not care which rows it has seen, then writes one partial per query head to
 // its slot and counts the visit in each head's visit count.  Faster CUs
 // simply take more units at the end.  Nothing here waits on another
@@ -588,7 +596,7 @@ __device__ int find_open_slab(const unsigned* __restrict__ cnt,
 //   slab line  per slab one 128-byte line: a 64-bit word {dynamic units
 //              taken (low), dynamic visits opened (high)}; reset by the merge
 //   nvis       [B][h_q] uint32 visits per query head; reset by the merge
-//   ws_ml      [B][h_q][J] float2        (running max, base-2 units; sum)
+//   ws_ml      [B][h_q][J] float2        (reference, base-2 units; sum)
 //   ws_acc     [B][h_q][J][DV]           unnormalised weighted sum of V rows
 // ---------------------------------------------------------------------------
 template <int DK, int DV, int NB, bool CAUSAL>

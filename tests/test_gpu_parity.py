@@ -160,6 +160,28 @@ def test_large_logits_stay_finite(cuda_device):
     check(got, ref, "large logits")
 
 
+@pytest.mark.parametrize("h_q", [8, 32], ids=["one_block", "two_blocks"])
+def test_rising_and_jumping_scores(cuda_device, h_q):
+    """Scores that climb steadily along the rows (about 100 base-2 units
+    over the sequence, so the softmax reference of the online form moves many
+    times, with weights of up to 2^8 between moves), then fall, then jump far
+    above everything before (a reference move that wipes the old weights)."""
+    n = 3000
+    shape = workloads.custom(f"rising_{h_q}", B=1, h_q=h_q, h_kv=1, d_k=128, d_v=128,
+                             n_max=n)
+    inp = workloads.make(shape, seed=31)
+    u = inp.q[0, 0].astype(np.float64)
+    u /= np.linalg.norm(u)
+    # log2-unit score of head 0 along u: log2(e) * scale * |q0| per unit of K
+    per_unit = np.log2(np.e) * shape.scale32() * np.linalg.norm(inp.q[0, 0].astype(np.float64))
+    ramp = np.concatenate([np.linspace(0.0, 100.0, 2000), np.linspace(100.0, 20.0, 999),
+                           [130.0]]) / per_unit
+    inp.K[0, 0, :n] += (ramp[:, None] * u[None, :]).astype(np.float32)
+    got = run_decode(inp, cuda_device)
+    ref = oracle.decode(inp.q, inp.K, inp.V, inp.lens, shape.scale32())
+    check(got, ref, f"rising scores h_q={h_q}")
+
+
 def test_plain_decode_leaves_cache_and_len_alone(cuda_device):
     shape = workloads.custom("plain", B=2, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=900)
     inp = workloads.make(shape, seed=9, lens=np.array([900, 450], np.int32))
