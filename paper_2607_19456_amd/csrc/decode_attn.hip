@@ -79,6 +79,12 @@ constexpr int kComputeUnits = 256;                   // MI355X
 // two-tile ring.
 template <int NB, int DK, int DV>
 constexpr int kRing = DK + DV > 256 ? 2 : (NB == 2 ? 4 : 3);
+// q of the visit's heads (the B operand of the score products) is held in
+// registers for the whole visit where they fit (NB * d_k / 4 per lane),
+// else re-read from LDS for every tile.  Two column blocks at d_k = 256
+// would need 128 registers for it.
+template <int NB, int DK>
+constexpr bool kPinQ = NB * DK <= 256;
 // A segment (chunk_rows) is the most rows a workgroup reads in one go from
 // its static range, a multiple of twelve 16-row tiles per wave (whole turns
 // of every ring); with no static share (single-chunk caches, very large
@@ -294,12 +300,16 @@ template <int DK, int DV, int NB, bool CAUSAL>
 __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0,
                                              const int (&lim)[NB], int k, int lane,
                                              const f4 (*__restrict__ sh_q)[DK / 16][kWave],
+                                             const f4 (&qr)[NB][DK / 16],
                                              float (&m_run)[NB], float (&l_run)[NB],
                                              f4 (&acc)[NB][DV / 64][4]) {
-  // q is re-read from LDS for every tile rather than pinned in 32 registers
-  // per column block, which are left to the load ring: the empty asm keeps
-  // the compiler from hoisting those reads out of the tile loop.
-  asm volatile("" ::: "memory");
+  // Unpinned, q is re-read from LDS for every tile: the empty asm keeps the
+  // compiler from hoisting those reads out of the tile loop.
+  if constexpr (!kPinQ<NB, DK>) asm volatile("" ::: "memory");
+  auto Q = [&](int nb, int t) -> f4 {
+    if constexpr (kPinQ<NB, DK>) return qr[nb][t];
+    else return sh_q[nb][t][lane];
+  };
   if constexpr (NB == 2) {
     // Both column blocks in step: their score chains (four independent
     // accumulators sharing each K operand), then both softmax updates, then
@@ -307,8 +317,8 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
     f4 sa0 = f4{0.f, 0.f, 0.f, 0.f}, sa1 = sa0, sb0 = sa0, sb1 = sa0;
 #pragma unroll
     for (int t = 0; t < DK / 16; t += 2) {
-      const f4 qa0 = sh_q[0][t][lane], qa1 = sh_q[0][t + 1][lane];
-      const f4 qb0 = sh_q[1][t][lane], qb1 = sh_q[1][t + 1][lane];
+      const f4 qa0 = Q(0, t), qa1 = Q(0, t + 1);
+      const f4 qb0 = Q(1, t), qb1 = Q(1, t + 1);
       sa0 = mfma_16x16x4(T.k[t].x, qa0.x, sa0);
       sb0 = mfma_16x16x4(T.k[t].x, qb0.x, sb0);
       sa1 = mfma_16x16x4(T.k[t + 1].x, qa1.x, sa1);
@@ -374,7 +384,7 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
   for (int nb = 0; nb < NB; ++nb) {
     f4 qb[DK / 16];
 #pragma unroll
-    for (int t = 0; t < DK / 16; ++t) qb[t] = sh_q[nb][t][lane];
+    for (int t = 0; t < DK / 16; ++t) qb[t] = Q(nb, t);
     // Step I: s[row 4k+r][head i] for the tile's 16 rows (two independent
     // accumulation chains over the d_k/4 steps, added at the end).
     f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
@@ -917,6 +927,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_partial_kernel(
       sh_q[e / (kWave * (DK / 16))][(e / kWave) % (DK / 16)][e % kWave] = qv[u] * qscale;
     }
     __syncthreads();
+    f4 qr[NB][DK / 16];
+    if constexpr (kPinQ<NB, DK>) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int t = 0; t < DK / 16; ++t) qr[nb][t] = sh_q[nb][t][lane];
+    }
 
     // Running state per column block; lane (k, i) belongs to head i.
     float m_run[NB], l_run[NB];
@@ -957,7 +974,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_partial_kernel(
             load_tile<DK, DV, NB, CAUSAL>(ring[(p + R - 1) % R], src, row_of(t + p + R - 1),
                                           last_row, i, k);
             if (r <= last_row)
-              process_tile<DK, DV, NB, CAUSAL>(ring[p], r, lim, k, lane, sh_q, m_run, l_run, acc);
+              process_tile<DK, DV, NB, CAUSAL>(ring[p], r, lim, k, lane, sh_q, qr, m_run, l_run,
+                                               acc);
           }
           t += R;
           // A wave whose remaining tiles all lie past the slab's end (only
