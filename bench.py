@@ -290,8 +290,8 @@ def main() -> int:
 
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU; --gpus {args.gpus} is not "
-              "supported (the decode would shard by KV head with no exchange, "
-              "see the design notes)", file=sys.stderr)
+              "supported (the decode would shard by KV head, each GPU holding whole "
+              "query-head groups, with no exchange between GPUs)", file=sys.stderr)
         return 2
 
     import numpy as np
