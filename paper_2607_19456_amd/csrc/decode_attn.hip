@@ -27,9 +27,10 @@
 //     scores  S[16 rows x 16 heads] = K_tile[16 x d_k] . Q^T[d_k x 16]
 //     update  O^T[d_v x 16 heads]  += V_tile^T[d_v x 16] . P[16 x 16 heads]
 //   with the online (running reference / running sum) form of the softmax
-//   between them, so the score vector never leaves registers.  Up to 16 query heads
-//   ride in one product's columns; groups of 17..32 heads use two column
-//   blocks over the same K/V registers, larger groups several head groups.
+//   between them, so the score vector never leaves registers.  Up to 16
+//   query heads ride in one product's columns; groups of 17..32 heads use
+//   two column blocks over the same K/V registers, larger groups several
+//   head groups.
 //   Scores are kept in base-2 units: q is pre-multiplied by scale*log2(e) and
 //   exponentials are exp2, which is the hardware's native exponential.
 //
