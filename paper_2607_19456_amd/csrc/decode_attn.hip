@@ -343,32 +343,49 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
     }
     f4 sc[2] = {sa0 + sa1, sb0 + sb1};
     f4 pr[2];
-    float alpha[2];
+    float tmax[2];
+    bool bump[2];
+    // Rows past the last row a column sees take no weight (only a slab's
+    // last tile has any, unless the columns are causal).
+    const bool mask = CAUSAL || row0 + kTileRows - 1 > lim[0];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
+      if (mask) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (row0 + 4 * k + r > lim[nb]) sc[nb][r] = -INFINITY;
-      const float tmax =
+        for (int r = 0; r < 4; ++r)
+          if (row0 + 4 * k + r > lim[nb]) sc[nb][r] = -INFINITY;
+      }
+      tmax[nb] =
           max_over_row_groups(fmaxf(fmaxf(sc[nb][0], sc[nb][1]), fmaxf(sc[nb][2], sc[nb][3])));
-      const float m_new = tmax > m_run[nb] + kLazyMax ? tmax : m_run[nb];
-      float m_ref = m_new;
-      if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
-      alpha[nb] = fast_exp2(m_run[nb] - m_ref);
+      bump[nb] = tmax[nb] > m_run[nb] + kLazyMax;
+    }
+    // A reference moves (rarely): rescale the sums of the heads it moves for.
+    if (__any(bump[0] || bump[1])) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const float m_new = bump[nb] ? tmax[nb] : m_run[nb];
+        float m_ref = m_new;
+        if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = fast_exp2(m_run[nb] - m_ref);
+        l_run[nb] *= alpha;
+#pragma unroll
+        for (int c = 0; c < DV / 64; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha;
+        m_run[nb] = m_new;
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      // A causal column may have seen no row yet (reference -inf):
+      // exponentiate against 0 then, so every weight is 0 instead of NaN.
+      float m_ref = m_run[nb];
+      if constexpr (CAUSAL) m_ref = m_ref == -INFINITY ? 0.f : m_ref;
       pr[nb][0] = fast_exp2(sc[nb][0] - m_ref);
       pr[nb][1] = fast_exp2(sc[nb][1] - m_ref);
       pr[nb][2] = fast_exp2(sc[nb][2] - m_ref);
       pr[nb][3] = fast_exp2(sc[nb][3] - m_ref);
-      l_run[nb] = l_run[nb] * alpha[nb] + ((pr[nb][0] + pr[nb][1]) + (pr[nb][2] + pr[nb][3]));
-      m_run[nb] = m_new;
-    }
-    if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int c = 0; c < DV / 64; ++c)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha[nb];
+      l_run[nb] += (pr[nb][0] + pr[nb][1]) + (pr[nb][2] + pr[nb][3]);
     }
 #pragma unroll
     for (int rho = 0; rho < 4; ++rho)
@@ -405,35 +422,41 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
       s1 = mfma_16x16x4(T.k[t + 1].w, qb[t + 1].w, s1);
     }
     f4 s = s0 + s1;
-    // Rows past the last row this lane's column sees take no weight.
+    // Rows past the last row this lane's column sees take no weight (only a
+    // slab's last tile has any, unless the columns are causal).
+    if (CAUSAL || row0 + kTileRows - 1 > lim[nb]) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (row0 + 4 * k + r > lim[nb]) s[r] = -INFINITY;
+      for (int r = 0; r < 4; ++r)
+        if (row0 + 4 * k + r > lim[nb]) s[r] = -INFINITY;
+    }
 
-    // Step II, online: the tile's max over the 4 row groups of head i, and
-    // the head's reference (raised only on a jump above kLazyMax).
+    // Step II, online: the tile's max over the 4 row groups of head i; the
+    // head's reference moves only on a jump above kLazyMax, and then (rarely)
+    // the sums are rescaled.
     const float tmax = max_over_row_groups(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
-    const float m_new = tmax > m_run[nb] + kLazyMax ? tmax : m_run[nb];
-    // A causal column may have seen no row yet (m_new = -inf): exponentiate
+    const bool bump = tmax > m_run[nb] + kLazyMax;
+    if (__any(bump)) {
+      const float m_new = bump ? tmax : m_run[nb];
+      float m_ref = m_new;
+      if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = fast_exp2(m_run[nb] - m_ref);
+      l_run[nb] *= alpha;
+#pragma unroll
+      for (int c = 0; c < DV / 64; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha;
+      m_run[nb] = m_new;
+    }
+    // A causal column may have seen no row yet (reference -inf): exponentiate
     // against 0 then, so every weight is 0 instead of NaN.
-    float m_ref = m_new;
-    if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run[nb] - m_ref);
+    float m_ref = m_run[nb];
+    if constexpr (CAUSAL) m_ref = m_ref == -INFINITY ? 0.f : m_ref;
     f4 pr;
     pr[0] = fast_exp2(s[0] - m_ref);
     pr[1] = fast_exp2(s[1] - m_ref);
     pr[2] = fast_exp2(s[2] - m_ref);
     pr[3] = fast_exp2(s[3] - m_ref);
-    l_run[nb] = l_run[nb] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
-    m_run[nb] = m_new;
-    // Most tiles leave every reference unchanged (alpha = 1 in every lane):
-    // skip the rescale of the accumulators then.
-    if (__any(alpha != 1.f)) {
-#pragma unroll
-      for (int c = 0; c < DV / 64; ++c)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[nb][c][e] *= alpha;
-    }
+    l_run[nb] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
 
     // Step III: acc += V_tile^T . P over rows {rho, 4+rho, 8+rho, 12+rho}.
 #pragma unroll
