@@ -1012,8 +1012,14 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
           // in the slab's last segment) leaves early instead of idling through
           // them.
         } while (t < ctpw && row_of(t) <= last_row);
-        if (tid == 0 && req) sh_next[it & 1] = after;
-        __syncthreads();
+        // Only a segment that requested a unit publishes it (and such
+        // segments are consecutive: the dynamic tail of the visit); the static
+        // segments before it need no barrier -- every wave derives the same
+        // segment stream by itself.
+        if (req) {
+          if (tid == 0) sh_next[it & 1] = after;
+          __syncthreads();
+        }
         cs = ns;
         ctpw = ntpw;
         if (cs < 0) break;
