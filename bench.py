@@ -335,13 +335,15 @@ def main() -> int:
     # (one launch writes the output): time da_decode_attn as a whole then.
     out = torch.empty((s.B, s.h_q) + ((s.rows,) if multi else ()) + (s.d_v,),
                       dtype=torch.float32, device=dev)
-    chunk = args.chunk_rows or binding.chunk_rows(s.B, s.h_q * s.rows, s.h_kv, s.n_max,
-                                                  s.d_k, s.d_v)
+    # The library's own segment size unless --chunk-rows asks for another
+    # (then the tuning calls run; `chunk` is reported either way).
+    ck = args.chunk_rows
+    chunk = ck or binding.chunk_rows(s.B, s.h_q * s.rows, s.h_kv, s.n_max, s.d_k, s.d_v)
     direct = not s.steps and not multi and chunk >= s.n_max
     if multi:
-        ws = binding.alloc_multi_workspace(dq[0], dK, dV, chunk)
+        ws = binding.alloc_multi_workspace(dq[0], dK, dV, ck)
     else:
-        ws = binding.alloc_workspace(dq[0], dK, dV, chunk)
+        ws = binding.alloc_workspace(dq[0], dK, dV, ck)
     scale = float(s.scale32())
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -360,25 +362,25 @@ def main() -> int:
             # several positions per step: da_decode_multi_step, both launches
             # inside the events
             binding.decode_multi_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=out,
-                                      workspace=ws, chunk_rows=chunk, stream=st)
+                                      workspace=ws, chunk_rows=ck, stream=st)
             if ev_b is not None:
                 ev_b.record(st)
             return
         if direct:
             binding.decode_attn(dq[t], dK, dV, dl, scale, out=out, workspace=ws,
-                                chunk_rows=chunk, stream=st)
+                                chunk_rows=ck, stream=st)
             if ev_b is not None:
                 ev_b.record(st)
             return
         if s.steps:
-            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk,
+            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, ck,
                                    k_new=dkn[t], v_new=dvn[t], stream=st)
         else:
-            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, chunk, stream=st)
+            binding.decode_partial(dq[t], dK, dV, dl, scale, ws, ck, stream=st)
         if ev_b is not None:
             ev_b.record(st)
         binding.decode_merge(out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
-                             chunk, lens=dl if s.steps else None, stream=st)
+                             ck, lens=dl if s.steps else None, stream=st)
 
     log(f"warmup {args.warmup} step(s), chunk_rows={chunk}")
     for i in range(args.warmup):

@@ -55,8 +55,8 @@ extern "C" {
 typedef enum da_status {
     DA_OK = 0,
     DA_ERR_NULL = 1,        /* a required pointer is NULL                          */
-    DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q,
-                               or chunk_rows not a positive multiple of 768        */
+    DA_ERR_SHAPE = 2,       /* a size < 1 or too large, h_kv not dividing h_q
+                               (or, tuning calls only, a bad chunk_rows)          */
     DA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {64, 128, 256} (decode), or not a
                                multiple of 4 (append)                              */
     DA_ERR_ALIGN = 4,       /* a float array not 16-byte aligned, len not 4-byte   */
@@ -65,8 +65,9 @@ typedef enum da_status {
     DA_ERR_HIP = 7          /* the HIP runtime reported an error at launch         */
 } da_status;
 
-/* Human-readable name of a status code (static string, never NULL). */
-const char *da_status_string(int status);
+/* Human-readable name of a status code (static string, never NULL; codes
+ * outside the enumeration give "unknown da_status"). */
+const char *da_status_string(da_status status);
 
 /*
  * Workspace.  The decode keeps, per (b, query head), a few partial results
@@ -74,37 +75,48 @@ const char *da_status_string(int status);
  * the sum of exponentials against it, the unnormalised weighted sum of V
  * rows) plus a few counters per (b, KV head) that schedule the work.  The
  * counter region -- the first da_decode_workspace_counter_bytes() bytes --
- * must be zero before the first decode that uses the workspace (an all-zero
- * workspace always qualifies); every completed decode leaves it zero again,
- * so a workspace can be reused call after call without clearing (and a call
- * can be captured in a HIP graph and replayed).  The rest of the workspace
- * needs no initialisation.  One workspace serves one decode at a time:
- * decodes that overlap in time (on different streams) need separate
+ * must be zero before a decode starts; every completed decode leaves it zero
+ * again, so a workspace can be reused call after call without clearing (and
+ * a call can be captured in a HIP graph and replayed).  A da_decode_partial
+ * that is not followed by its da_decode_merge (or a stream torn down between
+ * the two) leaves counters set: the next decode on that workspace would then
+ * skip rows, so such a workspace must be cleared first, with
+ * da_decode_workspace_reset or by zeroing the counter region.  The rest of
+ * the workspace needs no initialisation.  One workspace serves one decode at
+ * a time: decodes that overlap in time (on different streams) need separate
  * workspaces.
  */
 
 /*
- * Rows per work segment the library picks for these shapes when chunk_rows
- * is 0 below (a positive multiple of 768).  Returns 0 if the shapes are
- * invalid.
- */
-int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
-
-/*
- * Bytes of device workspace da_decode_attn / da_decode_step /
- * da_decode_partial + da_decode_merge need for these shapes and chunk size
- * (0 = the library's choice).  Returns 0 if the shapes or chunk_rows are
- * invalid.
+ * Bytes of device workspace da_decode_attn, da_decode_step and the
+ * da_decode_partial + da_decode_merge pair need for these shapes (the
+ * library chooses its work decomposition; the size covers every device the
+ * library runs on).  Returns 0 if the shapes are invalid.
  */
 size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
-                                 int d_v, int chunk_rows);
+                                 int d_v);
 
 /*
  * Leading bytes of that workspace that hold the scheduling counters (the part
- * that must be zero before first use).  Returns 0 if the shapes are invalid.
+ * that must be zero when a decode starts).  Returns 0 if the shapes are
+ * invalid.
  */
 size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
                                          int d_k, int d_v);
+
+/*
+ * Clears the counter region of a workspace for decodes of these shapes (h_q
+ * counts query rows: h_q*T for the T-row calls), with a kernel on `stream`
+ * (no memset node, so it can sit inside a captured HIP graph).  For
+ * recovering a workspace left by a partial without its merge; a workspace
+ * that only ever saw complete decodes never needs it.
+ * Errors: DA_ERR_NULL (workspace NULL), DA_ERR_SHAPE / DA_ERR_UNSUPPORTED
+ * (shapes), DA_ERR_WORKSPACE (workspace_bytes below the counter region),
+ * DA_ERR_ALIGN (workspace not 16-byte aligned), DA_ERR_HIP.
+ */
+da_status da_decode_workspace_reset(void *workspace, size_t workspace_bytes,
+                                    int B, int h_q, int h_kv, int n_max,
+                                    int d_k, int d_v, void *stream);
 
 /*
  * Decode attention, eqs. (1)-(3) (Algorithm 1) for every batch b and query
@@ -118,26 +130,26 @@ size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max,
  *
  * A resident set of workgroups shares the rows of all (b, KV head) slabs:
  * most of each slab in row ranges fixed in advance (proportional to the
- * lengths), the rest in small units handed out dynamically; a workgroup reads
- * its rows in segments of up to chunk_rows rows (0 = the library's choice),
+ * lengths), the rest in small units handed out dynamically; a workgroup
  * folds everything it reads from one slab into one running softmax state
  * (the online form of eq. (2)) and leaves one partial per visit; a second
  * launch combines the partials exactly (a regrouping of eqs. (2)-(3) over
  * disjoint row sets).  Which workgroup takes which dynamic unit varies, so
  * the summation order varies from call to call within fp32 rounding.  When
- * every slab fits in one segment the decode is a single launch that writes
- * out directly.  Equivalent to da_decode_partial followed by
- * da_decode_merge.
+ * every slab is short the decode is a single launch that writes out
+ * directly.  Equivalent to da_decode_partial followed by da_decode_merge.
  *
  * Supported: d_k, d_v in {64, 128, 256}; any B, h_q, h_kv >= 1 with h_kv | h_q.
  * workspace: see above; at least da_decode_workspace_bytes(...) bytes,
  * 16-byte aligned.  out must not overlap the inputs.
+ * Errors, checked in this order: DA_ERR_NULL (q, K, V, len, out), DA_ERR_SHAPE,
+ * DA_ERR_UNSUPPORTED, DA_ERR_ALIGN, DA_ERR_SCALE, DA_ERR_WORKSPACE, then
+ * DA_ERR_HIP from the launch.
  */
 da_status da_decode_attn(const float *q, const float *K, const float *V,
                          const int32_t *len, float scale, float *out, int B,
                          int h_q, int h_kv, int n_max, int d_k, int d_v,
-                         int chunk_rows, void *workspace,
-                         size_t workspace_bytes, void *stream);
+                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Append and decode in one step: the effect of da_kv_append(K, V, k_new,
@@ -152,38 +164,38 @@ da_status da_decode_attn(const float *q, const float *K, const float *V,
 da_status da_decode_step(const float *q, float *K, float *V,
                          const float *k_new, const float *v_new, int32_t *len,
                          float scale, float *out, int B, int h_q, int h_kv,
-                         int n_max, int d_k, int d_v, int chunk_rows,
-                         void *workspace, size_t workspace_bytes, void *stream);
+                         int n_max, int d_k, int d_v, void *workspace,
+                         size_t workspace_bytes, void *stream);
 
 /*
  * First half of da_decode_attn / da_decode_step: scores of all G query heads
  * of each group over the slab's rows (K and V rows read from HBM once per
  * (b, KV head)), their reference scores, sums of exponentials and
- * unnormalised weighted sums of V rows, written to the workspace as per-visit partials.
- * k_new and v_new are both NULL (plain decode; K and V are only read) or both
- * set (the fused append of da_decode_step: row len[b] of every KV head is
- * taken from them and written into K / V).  Must be followed by
- * da_decode_merge on the same workspace, which also resets the counters.
+ * unnormalised weighted sums of V rows, written to the workspace as per-visit
+ * partials.  k_new and v_new are both NULL (plain decode; K and V are only
+ * read) or both set (the fused append of da_decode_step: row len[b] of every
+ * KV head is taken from them and written into K / V).  Must be followed by
+ * da_decode_merge on the same workspace and stream, which also resets the
+ * counters (see the workspace notes above for a partial left without it).
  */
 da_status da_decode_partial(const float *q, float *K, float *V,
                             const float *k_new, const float *v_new,
                             const int32_t *len, float scale, int B, int h_q,
                             int h_kv, int n_max, int d_k, int d_v,
-                            int chunk_rows, void *workspace,
-                            size_t workspace_bytes, void *stream);
+                            void *workspace, size_t workspace_bytes,
+                            void *stream);
 
 /*
  * Second half: combines the partials of every (b, query head) into
  * out[b,h,:] (largest reference, rescaled sums, one division) and resets the
- * workspace counters to zero.  chunk_rows and the shapes must be those of the
+ * workspace counters to zero.  The shapes must be those of the
  * da_decode_partial call that filled the workspace.  len is NULL after a
  * plain decode; after a partial with a fused append it is that call's len,
  * and every len[b] with 0 <= len[b] < n_max advances by one.
  */
 da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
-                          int n_max, int d_k, int d_v, int chunk_rows,
-                          void *workspace, size_t workspace_bytes,
-                          void *stream);
+                          int n_max, int d_k, int d_v, void *workspace,
+                          size_t workspace_bytes, void *stream);
 
 /*
  * Decode with T query rows per query head (T >= 1): the rank-2 query of the
@@ -191,8 +203,8 @@ da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
  * (+.x Omega<2,2>) V, for a step that submits T consecutive positions at
  * once (speculative verification, chunked prefill), with causal visibility:
  * query row r of sequence b sits at cache position p = clamp(len[b], 0,
- * n_max) - T + r and attends rows 0..p; a row with p < 0 gives 0.  T = 1 is
- * da_decode_attn.
+ * n_max) - T + r (the cache's last T positions) and attends rows 0..p; a row
+ * with p < 0 gives 0.  T = 1 is da_decode_attn.
  *     q   float [B][h_q][T][d_k]      out float [B][h_q][T][d_v]
  * The T rows of every query head of a group are scored from the same K/V
  * reads (the kernels treat them as h_q*T query heads), so the workspace is
@@ -204,8 +216,7 @@ da_status da_decode_merge(float *out, int32_t *len, int B, int h_q, int h_kv,
 da_status da_decode_multi(const float *q, const float *K, const float *V,
                           const int32_t *len, float scale, float *out, int B,
                           int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
-                          int chunk_rows, void *workspace,
-                          size_t workspace_bytes, void *stream);
+                          void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * T autoregressive steps in one: the effect of T successive da_decode_step
@@ -215,13 +226,22 @@ da_status da_decode_multi(const float *q, const float *K, const float *V,
  * 0 .. min(len[b] + r, n_max - 1) of the grown cache (len[b] the value on
  * entry; nothing if len[b] < 0).  Two launches; len advances by the rows
  * that fit.  Workspace as da_decode_multi.
+ *
+ * While every row fits (0 <= len[b] and len[b] + T <= n_max) this equals
+ * da_kv_append_rows followed by da_decode_multi.  Near capacity the two
+ * differ on purpose: here row r still attends the rows a single step r
+ * would see (rows that did not fit are simply absent), whereas
+ * da_decode_multi places its T rows at the cache's last T positions.  E.g.
+ * len[b] = n_max - 2, T = 4: here rows 0..3 attend up to n_max-2, n_max-1,
+ * n_max-1, n_max-1; after da_kv_append_rows, da_decode_multi's rows attend
+ * up to n_max-4 .. n_max-1.
  */
 da_status da_decode_multi_step(const float *q, float *K, float *V,
                                const float *k_new, const float *v_new,
                                int32_t *len, float scale, float *out, int B,
                                int h_q, int h_kv, int n_max, int d_k, int d_v,
-                               int T, int chunk_rows, void *workspace,
-                               size_t workspace_bytes, void *stream);
+                               int T, void *workspace, size_t workspace_bytes,
+                               void *stream);
 
 /*
  * KV-cache append, eqs. (6)-(7) (K_{t+1} = K_t # k_t, V_{t+1} = V_t # v_t,
@@ -245,6 +265,56 @@ da_status da_kv_append(float *K, float *V, const float *k_new,
 da_status da_kv_append_rows(float *K, float *V, const float *k_new,
                             const float *v_new, int32_t *len, int B, int h_kv,
                             int n_max, int d_k, int d_v, int T, void *stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Tuning and testing only.  The entry points above choose their own segment
+ * size (the most rows a workgroup reads from its static range in one go,
+ * and for caches scheduled without a static share also the unit handed out
+ * dynamically).  These variants take it explicitly as chunk_rows, a positive
+ * multiple of 768 (0 = the library's choice), for sweeps and for tests that
+ * force a decomposition; results are the same decode within fp32 rounding.
+ * Not a stable interface: the decomposition may change without notice.
+ * A workspace sized by da_decode_workspace_bytes_ex for some chunk_rows
+ * serves only calls with that chunk_rows.  DA_ERR_SHAPE also covers an
+ * invalid chunk_rows.
+ * ---------------------------------------------------------------------------
+ */
+
+/* Segment rows the entry points above pick for these shapes (a positive
+ * multiple of 768; for the T-row calls pass h_q*T).  0 if the shapes are
+ * invalid. */
+int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v);
+
+/* Workspace bytes for chunk_rows (0 = the library's choice, which gives
+ * da_decode_workspace_bytes).  0 if the shapes or chunk_rows are invalid. */
+size_t da_decode_workspace_bytes_ex(int B, int h_q, int h_kv, int n_max,
+                                    int d_k, int d_v, int chunk_rows);
+
+/* da_decode_multi (T = 1: da_decode_attn) with an explicit chunk_rows. */
+da_status da_decode_multi_ex(const float *q, const float *K, const float *V,
+                             const int32_t *len, float scale, float *out,
+                             int B, int h_q, int h_kv, int n_max, int d_k,
+                             int d_v, int T, int chunk_rows, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/* da_decode_partial for T query rows per head (causal, as da_decode_multi;
+ * with k_new / v_new the T-row append of da_decode_multi_step) with an
+ * explicit chunk_rows. */
+da_status da_decode_partial_ex(const float *q, float *K, float *V,
+                               const float *k_new, const float *v_new,
+                               const int32_t *len, float scale, int B,
+                               int h_q, int h_kv, int n_max, int d_k, int d_v,
+                               int T, int chunk_rows, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
+/* da_decode_merge for T query rows per head with an explicit chunk_rows (the
+ * T and chunk_rows of the partial that filled the workspace; len advances by
+ * the rows that fit). */
+da_status da_decode_merge_ex(float *out, int32_t *len, int B, int h_q,
+                             int h_kv, int n_max, int d_k, int d_v, int T,
+                             int chunk_rows, void *workspace,
+                             size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -27,17 +27,23 @@ STATUS = {
 _vp, _ci, _cf, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 SIGNATURES = {
     "da_status_string": (ctypes.c_char_p, [_ci]),
-    "da_decode_chunk_rows": (_ci, [_ci] * 6),
-    "da_decode_workspace_bytes": (_sz, [_ci] * 7),
+    "da_decode_workspace_bytes": (_sz, [_ci] * 6),
     "da_decode_workspace_counter_bytes": (_sz, [_ci] * 6),
-    "da_decode_attn": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_partial": (_ci, [_vp] * 6 + [_cf] + [_ci] * 7 + [_vp, _sz, _vp]),
-    "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_workspace_reset": (_ci, [_vp, _sz] + [_ci] * 6 + [_vp]),
+    "da_decode_attn": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 6 + [_vp, _sz, _vp]),
+    "da_decode_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 6 + [_vp, _sz, _vp]),
+    "da_decode_partial": (_ci, [_vp] * 6 + [_cf] + [_ci] * 6 + [_vp, _sz, _vp]),
+    "da_decode_merge": (_ci, [_vp, _vp] + [_ci] * 6 + [_vp, _sz, _vp]),
+    "da_decode_multi": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
+    "da_decode_multi_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
-    "da_decode_multi": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
-    "da_decode_multi_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
     "da_kv_append_rows": (_ci, [_vp] * 5 + [_ci] * 6 + [_vp]),
+    # tuning and testing only (explicit segment size)
+    "da_decode_chunk_rows": (_ci, [_ci] * 6),
+    "da_decode_workspace_bytes_ex": (_sz, [_ci] * 7),
+    "da_decode_multi_ex": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
+    "da_decode_partial_ex": (_ci, [_vp] * 6 + [_cf] + [_ci] * 8 + [_vp, _sz, _vp]),
+    "da_decode_merge_ex": (_ci, [_vp, _vp] + [_ci] * 8 + [_vp, _sz, _vp]),
 }
 
 
@@ -88,18 +94,30 @@ def _stream(stream) -> int:
 
 
 def chunk_rows(B, h_q, h_kv, n_max, d_k, d_v) -> int:
-    """Rows per work chunk the library picks for these shapes (0: invalid)."""
+    """Segment rows the library picks for these shapes (0: invalid); tuning only."""
     return int(_lib.da_decode_chunk_rows(B, h_q, h_kv, n_max, d_k, d_v))
 
 
 def workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows: int = 0) -> int:
-    """Workspace bytes a decode with these shapes and chunk size needs."""
-    return int(_lib.da_decode_workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows))
+    """Workspace bytes a decode with these shapes needs (``chunk_rows`` != 0:
+    for the tuning calls with that segment size)."""
+    if chunk_rows:
+        return int(_lib.da_decode_workspace_bytes_ex(B, h_q, h_kv, n_max, d_k, d_v,
+                                                     chunk_rows))
+    return int(_lib.da_decode_workspace_bytes(B, h_q, h_kv, n_max, d_k, d_v))
 
 
 def workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, d_v) -> int:
     """Leading workspace bytes that must be zero before first use."""
     return int(_lib.da_decode_workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, d_v))
+
+
+def workspace_reset(workspace, B, h_q, h_kv, n_max, d_k, d_v, stream=None) -> None:
+    """Zero the counter region of ``workspace`` (h_q counts query rows, h_q*T
+    for the T-row calls) with a kernel on the stream."""
+    wp, wn = _ws(workspace)
+    _check("da_decode_workspace_reset", _lib.da_decode_workspace_reset(
+        wp, wn, B, h_q, h_kv, n_max, d_k, d_v, _stream(stream)))
 
 
 def _shapes(q, K, V):
@@ -131,38 +149,47 @@ def _ws(ws):
 
 def decode_attn(q, K, V, lens, scale: float, out=None, workspace=None,
                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
-    """out[b,h,:] = softmax(scale * K[b,g] q[b,h]) V[b,g] over len[b] rows."""
+    """out[b,h,:] = softmax(scale * K[b,g] q[b,h]) V[b,g] over len[b] rows
+    (``chunk_rows`` != 0: the tuning call with that segment size)."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     if out is None:
         out = torch.empty((B, h_q, d_v), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = alloc_workspace(q, K, V, chunk_rows)
     wp, wn = _ws(workspace)
-    _check("da_decode_attn", _lib.da_decode_attn(
-        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
-        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
-        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
-        d_v, int(chunk_rows), wp, wn, _stream(stream)))
+    args = (_dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+            _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+            float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k, d_v)
+    if chunk_rows:
+        _check("da_decode_multi_ex", _lib.da_decode_multi_ex(
+            *args, 1, int(chunk_rows), wp, wn, _stream(stream)))
+    else:
+        _check("da_decode_attn", _lib.da_decode_attn(*args, wp, wn, _stream(stream)))
     return out
 
 
 def decode_step(q, K, V, k_new, v_new, lens, scale: float, out=None, workspace=None,
                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
     """kv_append(K, V, k_new, v_new, lens) then decode_attn(q, K, V, lens),
-    fused into two kernel launches."""
+    fused into two kernel launches (``chunk_rows`` != 0: the same two
+    launches through the tuning calls)."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
     if out is None:
         out = torch.empty((B, h_q, d_v), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = alloc_workspace(q, K, V, chunk_rows)
+    if chunk_rows:
+        decode_partial(q, K, V, lens, scale, workspace, chunk_rows, k_new, v_new, stream)
+        return decode_merge(out, workspace, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
+                            lens, stream)
     wp, wn = _ws(workspace)
     _check("da_decode_step", _lib.da_decode_step(
         _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
         _dev(V, "V", torch.float32), _dev(k_new, "k_new", torch.float32),
         _dev(v_new, "v_new", torch.float32), _dev(lens, "len", torch.int32),
         float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
-        d_v, int(chunk_rows), wp, wn, _stream(stream)))
+        d_v, wp, wn, _stream(stream)))
     return out
 
 
@@ -172,33 +199,50 @@ def _new_rows(k_new, v_new, B, h_kv, d_k, d_v):
 
 
 def decode_partial(q, K, V, lens, scale: float, workspace, chunk_rows: int = 0,
-                   k_new=None, v_new=None, stream=None) -> None:
+                   k_new=None, v_new=None, stream=None, T: int = 1) -> None:
     """Partials of the decode into ``workspace`` (follow with decode_merge).
-    With ``k_new``/``v_new`` the partial also performs the fused append."""
-    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    With ``k_new``/``v_new`` the partial also performs the fused append.
+    ``T`` > 1 or ``chunk_rows`` != 0 go through the tuning call
+    (q [B,h_q,T,d_k], k_new/v_new [B,h_kv,T,d] then)."""
+    if T == 1 and q.dim() == 3:
+        B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    else:
+        B, h_q, h_kv, n_max, d_k, d_v, T = _multi_shapes(q, K, V)
     wp, wn = _ws(workspace)
     kp = vp = None
     if k_new is not None or v_new is not None:
-        _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
+        if T == 1 and k_new.dim() == 3:
+            _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
+        elif (tuple(k_new.shape) != (B, h_kv, T, d_k)
+              or tuple(v_new.shape) != (B, h_kv, T, d_v)):
+            raise ValueError("k_new must be [B,h_kv,T,d_k] and v_new [B,h_kv,T,d_v]")
         kp = _dev(k_new, "k_new", torch.float32)
         vp = _dev(v_new, "v_new", torch.float32)
-    _check("da_decode_partial", _lib.da_decode_partial(
-        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
-        _dev(V, "V", torch.float32), kp, vp, _dev(lens, "len", torch.int32),
-        float(scale), B, h_q, h_kv, n_max, d_k, d_v, int(chunk_rows), wp, wn,
-        _stream(stream)))
+    args = (_dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+            _dev(V, "V", torch.float32), kp, vp, _dev(lens, "len", torch.int32),
+            float(scale), B, h_q, h_kv, n_max, d_k, d_v)
+    if T != 1 or chunk_rows:
+        _check("da_decode_partial_ex", _lib.da_decode_partial_ex(
+            *args, int(T), int(chunk_rows), wp, wn, _stream(stream)))
+    else:
+        _check("da_decode_partial", _lib.da_decode_partial(*args, wp, wn, _stream(stream)))
 
 
 def decode_merge(out, workspace, B, h_q, h_kv, n_max, d_k, d_v,
-                 chunk_rows: int = 0, lens=None, stream=None) -> torch.Tensor:
+                 chunk_rows: int = 0, lens=None, stream=None, T: int = 1) -> torch.Tensor:
     """Combine the partials in ``workspace`` into ``out`` (re-zeroes the
     workspace counters).  ``lens``: after a partial with a fused append, the
-    lengths to advance by one."""
+    lengths to advance.  ``T`` and ``chunk_rows``: those of the partial."""
     wp, wn = _ws(workspace)
     lp = None if lens is None else _dev(lens, "len", torch.int32)
-    _check("da_decode_merge", _lib.da_decode_merge(
-        _dev(out, "out", torch.float32), lp, B, h_q, h_kv, n_max, d_k, d_v,
-        int(chunk_rows), wp, wn, _stream(stream)))
+    op = _dev(out, "out", torch.float32)
+    if T != 1 or chunk_rows:
+        _check("da_decode_merge_ex", _lib.da_decode_merge_ex(
+            op, lp, B, h_q, h_kv, n_max, d_k, d_v, int(T), int(chunk_rows), wp, wn,
+            _stream(stream)))
+    else:
+        _check("da_decode_merge", _lib.da_decode_merge(
+            op, lp, B, h_q, h_kv, n_max, d_k, d_v, wp, wn, _stream(stream)))
     return out
 
 
@@ -249,11 +293,15 @@ def decode_multi(q, K, V, lens, scale: float, out=None, workspace=None,
     if workspace is None:
         workspace = alloc_multi_workspace(q, K, V, chunk_rows)
     wp, wn = _ws(workspace)
-    _check("da_decode_multi", _lib.da_decode_multi(
-        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
-        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
-        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
-        d_v, T, int(chunk_rows), wp, wn, _stream(stream)))
+    args = (_dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+            _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+            float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
+            d_v, T)
+    if chunk_rows:
+        _check("da_decode_multi_ex", _lib.da_decode_multi_ex(
+            *args, int(chunk_rows), wp, wn, _stream(stream)))
+    else:
+        _check("da_decode_multi", _lib.da_decode_multi(*args, wp, wn, _stream(stream)))
     return out
 
 
@@ -268,13 +316,17 @@ def decode_multi_step(q, K, V, k_new, v_new, lens, scale: float, out=None,
         out = torch.empty((B, h_q, T, d_v), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = alloc_multi_workspace(q, K, V, chunk_rows)
+    if chunk_rows:
+        decode_partial(q, K, V, lens, scale, workspace, chunk_rows, k_new, v_new, stream, T)
+        return decode_merge(out, workspace, B, h_q, h_kv, n_max, d_k, d_v, chunk_rows,
+                            lens, stream, T)
     wp, wn = _ws(workspace)
     _check("da_decode_multi_step", _lib.da_decode_multi_step(
         _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
         _dev(V, "V", torch.float32), _dev(k_new, "k_new", torch.float32),
         _dev(v_new, "v_new", torch.float32), _dev(lens, "len", torch.int32),
         float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k,
-        d_v, T, int(chunk_rows), wp, wn, _stream(stream)))
+        d_v, T, wp, wn, _stream(stream)))
     return out
 
 

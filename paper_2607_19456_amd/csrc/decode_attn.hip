@@ -43,6 +43,7 @@
 
 #include <cmath>
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
 
 #include "decode_attn.h"
@@ -66,7 +67,11 @@ constexpr float kLazyMax = 8.f;
 constexpr int kHeadsPerBlock = 16;                   // heads per MFMA column block
 constexpr int kMaxHeadBlocks = 2;                    // column blocks per workgroup
 constexpr int kHeadsPerGroup = kHeadsPerBlock * kMaxHeadBlocks;
-constexpr int kComputeUnits = 256;                   // MI355X
+// Resident workgroups of the partial kernel: one per compute unit of the
+// current device (hipDeviceAttributeMultiprocessorCount), at most this many
+// -- the most CUs a gfx950 part has (MI355X: 256).  Workspace sizes are
+// computed for this bound, so they hold on any device the library runs on.
+constexpr int kMaxResident = 256;
 // Register tiles per wave in the load ring of the partial kernel, which
 // runs one wave per SIMD (all 512 registers of a lane).  One column block
 // (<= 16 query rows per KV head): a three-tile ring keeps two tiles' loads in
@@ -1245,8 +1250,37 @@ da_status check_shapes(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
   return DA_OK;
 }
 
+// Resident workgroups on the current device: its compute units, at most
+// kMaxResident, queried once per device.  Without a device (the call can then
+// only fail at launch) the bound itself.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_device_cus[kMaxDevices];
+
+int device_resident() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return kMaxResident;
+  }
+  int c = g_device_cus[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n < 1) {
+      (void)hipGetLastError();
+      return kMaxResident;
+    }
+    c = std::min(n, kMaxResident);
+    g_device_cus[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
+// The work decomposition for these shapes with `resident` resident
+// workgroups.  Every size below grows with `resident`, so the plan for
+// kMaxResident bounds the workspace of any device's plan.
 da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
-                    Plan* plan) {
+                    int resident, Plan* plan) {
   da_status st = check_shapes(B, h_q, h_kv, n_max, d_k, d_v);
   if (st != DA_OK) return st;
   const int G = h_q / h_kv;
@@ -1265,8 +1299,7 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int64_t chunks_per_slab = ceil_div(n_max, chunk_rows);
   plan->single_chunk = chunks_per_slab == 1;
   // One resident workgroup per CU, fewer if there are fewer chunks than that.
-  const int64_t resident = kComputeUnits;
-  plan->grid = (int)std::max<int64_t>(1, std::min(resident, chunks_per_slab * plan->slabs));
+  plan->grid = (int)std::max<int64_t>(1, std::min<int64_t>(resident, chunks_per_slab * plan->slabs));
   // Static share: off for single-chunk caches (direct form) and for batches
   // whose per-workgroup prefix over sequences would be long.  With two or
   // more slabs per workgroup the even split of whole slabs balances the
@@ -1390,8 +1423,10 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
   if ((k_new == nullptr) != (v_new == nullptr)) return DA_ERR_NULL;
   const int rows = query_rows(h_q, T);
   if (rows < 0 || h_q < 1) return DA_ERR_SHAPE;
+  // Validated against the documented size (the plan for kMaxResident), run
+  // with the device's own plan (never larger).
   Plan pl;
-  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
+  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, kMaxResident, &pl);
   if (st != DA_OK) return st;
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4) ||
       !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(out, 16))
@@ -1399,6 +1434,7 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
   if (!std::isfinite(scale)) return DA_ERR_SCALE;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
+  (void)make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, device_resident(), &pl);
   if (out_plan) *out_plan = pl;
 
   const WsView w = view(pl, workspace);
@@ -1429,11 +1465,12 @@ da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, in
   const int rows = query_rows(h_q, T);
   if (rows < 0 || h_q < 1) return DA_ERR_SHAPE;
   Plan pl;
-  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, &pl);
+  da_status st = make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, kMaxResident, &pl);
   if (st != DA_OK) return st;
   if (!aligned(out, 16) || !aligned(len_bump, 4)) return DA_ERR_ALIGN;
   if (!workspace || workspace_bytes < pl.bytes) return DA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
+  (void)make_plan(B, rows, h_kv, n_max, d_k, d_v, chunk_rows, device_resident(), &pl);
 
   const WsView w = view(pl, workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1455,12 +1492,29 @@ da_status merge_impl(float* out, int32_t* len_bump, int B, int h_q, int h_kv, in
   return launch_status();
 }
 
+// Zeroes n bytes (a multiple of 16) at p: the workspace counter reset, as a
+// kernel rather than a memset so that it can be captured in a graph.
+__global__ __launch_bounds__(kThreads) void clear_kernel(u4* __restrict__ p, size_t n16) {
+  for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n16;
+       e += (size_t)gridDim.x * kThreads)
+    p[e] = u4{0u, 0u, 0u, 0u};
+}
+
+da_status clear_words(void* p, size_t bytes, hipStream_t s) {
+  const size_t n16 = bytes / 16;
+  const unsigned grid = (unsigned)std::min<size_t>(1024, (n16 + kThreads - 1) / kThreads);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(clear_kernel, dim3(std::max(grid, 1u)), dim3(kThreads), 0, s,
+                     static_cast<u4*>(p), n16);
+  return launch_status();
+}
+
 }  // namespace
 
 extern "C" {
 
-const char* da_status_string(int status) {
-  switch (status) {
+const char* da_status_string(da_status status) {
+  switch ((int)status) {
     case DA_OK: return "DA_OK";
     case DA_ERR_NULL: return "DA_ERR_NULL: a required pointer is NULL";
     case DA_ERR_SHAPE: return "DA_ERR_SHAPE: invalid sizes or chunk_rows";
@@ -1473,80 +1527,75 @@ const char* da_status_string(int status) {
   }
 }
 
-int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
-  Plan pl;
-  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, &pl) != DA_OK) return 0;
-  return pl.chunk_rows;
-}
-
-size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
-                                 int chunk_rows) {
-  Plan pl;
-  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, &pl) != DA_OK) return 0;
-  return pl.bytes;
+size_t da_decode_workspace_bytes(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
+  return da_decode_workspace_bytes_ex(B, h_q, h_kv, n_max, d_k, d_v, 0);
 }
 
 size_t da_decode_workspace_counter_bytes(int B, int h_q, int h_kv, int n_max, int d_k,
                                          int d_v) {
   Plan pl;
-  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, &pl) != DA_OK) return 0;
+  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, kMaxResident, &pl) != DA_OK) return 0;
   return pl.counter_bytes;
 }
 
-da_status da_decode_partial(const float* q, float* K, float* V, const float* k_new,
-                            const float* v_new, const int32_t* len, float scale, int B,
-                            int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
-                            void* workspace, size_t workspace_bytes, void* stream) {
-  return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v, 1,
-                      chunk_rows, workspace, workspace_bytes, stream, nullptr, false, nullptr);
-}
-
-da_status da_decode_merge(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
-                          int d_k, int d_v, int chunk_rows, void* workspace,
-                          size_t workspace_bytes, void* stream) {
-  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, 1, chunk_rows, workspace,
-                    workspace_bytes, stream);
+da_status da_decode_workspace_reset(void* workspace, size_t workspace_bytes, int B, int h_q,
+                                    int h_kv, int n_max, int d_k, int d_v, void* stream) {
+  if (!workspace) return DA_ERR_NULL;
+  Plan pl;
+  const da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, kMaxResident, &pl);
+  if (st != DA_OK) return st;
+  if (workspace_bytes < pl.counter_bytes) return DA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return DA_ERR_ALIGN;
+  return clear_words(workspace, pl.counter_bytes, static_cast<hipStream_t>(stream));
 }
 
 da_status da_decode_attn(const float* q, const float* K, const float* V, const int32_t* len,
                          float scale, float* out, int B, int h_q, int h_kv, int n_max,
-                         int d_k, int d_v, int chunk_rows, void* workspace,
-                         size_t workspace_bytes, void* stream) {
-  return da_decode_multi(q, K, V, len, scale, out, B, h_q, h_kv, n_max, d_k, d_v, 1,
-                         chunk_rows, workspace, workspace_bytes, stream);
+                         int d_k, int d_v, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  return da_decode_multi_ex(q, K, V, len, scale, out, B, h_q, h_kv, n_max, d_k, d_v, 1, 0,
+                            workspace, workspace_bytes, stream);
 }
 
 da_status da_decode_step(const float* q, float* K, float* V, const float* k_new,
                          const float* v_new, int32_t* len, float scale, float* out, int B,
-                         int h_q, int h_kv, int n_max, int d_k, int d_v, int chunk_rows,
-                         void* workspace, size_t workspace_bytes, void* stream) {
+                         int h_q, int h_kv, int n_max, int d_k, int d_v, void* workspace,
+                         size_t workspace_bytes, void* stream) {
   return da_decode_multi_step(q, K, V, k_new, v_new, len, scale, out, B, h_q, h_kv, n_max,
-                              d_k, d_v, 1, chunk_rows, workspace, workspace_bytes, stream);
+                              d_k, d_v, 1, workspace, workspace_bytes, stream);
+}
+
+da_status da_decode_partial(const float* q, float* K, float* V, const float* k_new,
+                            const float* v_new, const int32_t* len, float scale, int B,
+                            int h_q, int h_kv, int n_max, int d_k, int d_v, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return da_decode_partial_ex(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
+                              1, 0, workspace, workspace_bytes, stream);
+}
+
+da_status da_decode_merge(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
+                          int d_k, int d_v, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return da_decode_merge_ex(out, len, B, h_q, h_kv, n_max, d_k, d_v, 1, 0, workspace,
+                            workspace_bytes, stream);
 }
 
 da_status da_decode_multi(const float* q, const float* K, const float* V, const int32_t* len,
                           float scale, float* out, int B, int h_q, int h_kv, int n_max,
-                          int d_k, int d_v, int T, int chunk_rows, void* workspace,
-                          size_t workspace_bytes, void* stream) {
-  Plan pl;
-  da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
-                              d_v, T, chunk_rows, workspace, workspace_bytes, stream, out, true,
-                              &pl, true);
-  if (st != DA_OK) return st;
-  if (pl.single_chunk) return DA_OK;                  // the direct form wrote out
-  return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
-                    workspace_bytes, stream);
+                          int d_k, int d_v, int T, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return da_decode_multi_ex(q, K, V, len, scale, out, B, h_q, h_kv, n_max, d_k, d_v, T, 0,
+                            workspace, workspace_bytes, stream);
 }
 
 da_status da_decode_multi_step(const float* q, float* K, float* V, const float* k_new,
                                const float* v_new, int32_t* len, float scale, float* out,
                                int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
-                               int chunk_rows, void* workspace, size_t workspace_bytes,
-                               void* stream) {
+                               void* workspace, size_t workspace_bytes, void* stream) {
   if (!k_new || !v_new) return DA_ERR_NULL;
   Plan pl;
   da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
-                              T, chunk_rows, workspace, workspace_bytes, stream, out, true, &pl);
+                              T, 0, workspace, workspace_bytes, stream, out, true, &pl);
   if (st != DA_OK) return st;
   return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
@@ -1574,6 +1623,52 @@ da_status da_kv_append(float* K, float* V, const float* k_new, const float* v_ne
                        int32_t* len, int B, int h_kv, int n_max, int d_k, int d_v,
                        void* stream) {
   return da_kv_append_rows(K, V, k_new, v_new, len, B, h_kv, n_max, d_k, d_v, 1, stream);
+}
+
+// --- tuning and testing only: explicit segment size -------------------------
+
+int da_decode_chunk_rows(int B, int h_q, int h_kv, int n_max, int d_k, int d_v) {
+  Plan pl;
+  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, kMaxResident, &pl) != DA_OK) return 0;
+  return pl.chunk_rows;
+}
+
+size_t da_decode_workspace_bytes_ex(int B, int h_q, int h_kv, int n_max, int d_k, int d_v,
+                                    int chunk_rows) {
+  Plan pl;
+  if (make_plan(B, h_q, h_kv, n_max, d_k, d_v, chunk_rows, kMaxResident, &pl) != DA_OK)
+    return 0;
+  return pl.bytes;
+}
+
+da_status da_decode_multi_ex(const float* q, const float* K, const float* V,
+                             const int32_t* len, float scale, float* out, int B, int h_q,
+                             int h_kv, int n_max, int d_k, int d_v, int T, int chunk_rows,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  da_status st = partial_impl(q, K, V, nullptr, nullptr, len, scale, B, h_q, h_kv, n_max, d_k,
+                              d_v, T, chunk_rows, workspace, workspace_bytes, stream, out, true,
+                              &pl, true);
+  if (st != DA_OK) return st;
+  if (pl.single_chunk) return DA_OK;                  // the direct form wrote out
+  return merge_impl(out, nullptr, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
+                    workspace_bytes, stream);
+}
+
+da_status da_decode_partial_ex(const float* q, float* K, float* V, const float* k_new,
+                               const float* v_new, const int32_t* len, float scale, int B,
+                               int h_q, int h_kv, int n_max, int d_k, int d_v, int T,
+                               int chunk_rows, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  return partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v, T,
+                      chunk_rows, workspace, workspace_bytes, stream, nullptr, false, nullptr);
+}
+
+da_status da_decode_merge_ex(float* out, int32_t* len, int B, int h_q, int h_kv, int n_max,
+                             int d_k, int d_v, int T, int chunk_rows, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, T, chunk_rows, workspace,
+                    workspace_bytes, stream);
 }
 
 }  // extern "C"

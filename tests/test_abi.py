@@ -25,9 +25,58 @@ def _declared():
     return set(re.findall(r"\b(da_[a-z_]+)\s*\(", text))
 
 
+# The boundary's core, exactly as specified: argument types in order
+# (pointers, scalars) and the result type.
+CORE_PROTOTYPES = {
+    "da_status_string": ("const char *", ["da_status"]),
+    "da_decode_workspace_bytes": ("size_t", ["int"] * 6),
+    "da_decode_attn": ("da_status", ["const float *"] * 3 + ["const int32_t *", "float",
+                                                              "float *"] + ["int"] * 6
+                       + ["void *", "size_t", "void *"]),
+    "da_kv_append": ("da_status", ["float *", "float *", "const float *", "const float *",
+                                   "int32_t *"] + ["int"] * 5 + ["void *"]),
+}
+
+
+def _norm(t):
+    """A C type with canonical spacing: 'const float*' -> 'const float *'."""
+    return " ".join(t.replace("*", " * ").split())
+
+
+def _prototypes():
+    """name -> (result type, [parameter types]) for every declaration in the
+    header (parameter names dropped)."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    protos = {}
+    for m in re.finditer(r"([A-Za-z_][\w \t\*]*?)\b(da_[a-z_]+)\s*\(([^)]*)\)\s*;", text):
+        params = []
+        for p in m.group(3).split(","):
+            toks = _norm(p).split(" ")
+            params.append(" ".join(toks[:-1]))          # drop the parameter name
+        protos[m.group(2)] = (_norm(m.group(1).split("\n")[-1]), params)
+    return protos
+
+
+def test_core_prototypes_are_exactly_the_specified_ones():
+    protos = _prototypes()
+    for name, (ret, params) in CORE_PROTOTYPES.items():
+        assert name in protos, name
+        got_ret, got_params = protos[name]
+        assert got_ret == _norm(ret), (name, got_ret)
+        assert got_params == [_norm(p) for p in params], (name, got_params)
+    # the tuning knob appears only in the tuning calls
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for m in re.finditer(r"\b(da_[a-z_]+)\s*\(([^)]*)\)\s*;", text):
+        if "chunk_rows" in m.group(2):
+            assert m.group(1).endswith("_ex"), m.group(1)
+
+
 def test_every_declared_symbol_is_exported():
     names = _declared()
     assert names == set(binding.SIGNATURES), names ^ set(binding.SIGNATURES)
+    protos = _prototypes()
+    for n, (_, params) in protos.items():
+        assert len(params) == len(binding.SIGNATURES[n][1]), n
     for n in names:
         assert hasattr(lib, n)
     out = subprocess.run(["nm", "-D", "--defined-only", binding.LIBRARY_PATH],
@@ -80,21 +129,27 @@ def test_chunk_rows_and_workspace_sizes():
         counters, total = _expected_workspace(*args, c)
         assert binding.workspace_counter_bytes(*args) == counters
         assert binding.workspace_bytes(*args) == total
+        assert lib.da_decode_workspace_bytes(*args) == total
+        assert lib.da_decode_workspace_bytes_ex(*args, 0) == total
         assert binding.workspace_bytes(*args, 1536) == _expected_workspace(*args, 1536)[1]
     assert binding.chunk_rows(1, 3, 2, 10, 64, 64) == 0       # h_kv does not divide h_q
     assert binding.workspace_bytes(1, 1, 1, 10, 96, 64) == 0  # unsupported d_k
     assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 192) == 0  # chunk not a multiple of 768
     assert binding.workspace_bytes(1, 1, 1, 10, 64, 64, 384) == 0
+    assert lib.da_decode_workspace_bytes(1, 3, 2, 10, 64, 64) == 0
 
 
 def _decode(**kw):
+    """da_decode_attn, or with ``chunk`` its tuning form da_decode_multi_ex."""
     a = dict(q=FAKE, K=FAKE, V=FAKE, len=FAKE, scale=0.125, out=FAKE, B=1, h_q=1,
-             h_kv=1, n_max=128, d_k=64, d_v=64, chunk=0, ws=FAKE, wsn=1 << 30,
+             h_kv=1, n_max=128, d_k=64, d_v=64, chunk=None, ws=FAKE, wsn=1 << 30,
              stream=None)
     a.update(kw)
-    return lib.da_decode_attn(a["q"], a["K"], a["V"], a["len"], a["scale"], a["out"],
-                              a["B"], a["h_q"], a["h_kv"], a["n_max"], a["d_k"],
-                              a["d_v"], a["chunk"], a["ws"], a["wsn"], a["stream"])
+    head = (a["q"], a["K"], a["V"], a["len"], a["scale"], a["out"], a["B"], a["h_q"],
+            a["h_kv"], a["n_max"], a["d_k"], a["d_v"])
+    if a["chunk"] is None:
+        return lib.da_decode_attn(*head, a["ws"], a["wsn"], a["stream"])
+    return lib.da_decode_multi_ex(*head, 1, a["chunk"], a["ws"], a["wsn"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -116,26 +171,45 @@ def test_decode_validation(kw, status):
 
 def test_partial_and_merge_validation():
     P = lib.da_decode_partial
-    assert P(None, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+    assert P(None, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64,
              FAKE, 1 << 20, None) == 1
-    assert P(FAKE, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+    assert P(FAKE, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64,
              FAKE, 8, None) == 6
     # k_new and v_new come together or not at all
-    assert P(FAKE, FAKE, FAKE, FAKE, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+    assert P(FAKE, FAKE, FAKE, FAKE, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64,
              FAKE, 1 << 20, None) == 1
-    assert P(FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0,
+    assert P(FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE, 0.1, 1, 1, 1, 64, 64, 64,
              FAKE, 1 << 20, None) == 4
     M = lib.da_decode_merge
-    assert M(None, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 1
-    assert M(FAKE, None, 1, 2, 3, 64, 64, 64, 0, FAKE, 1 << 20, None) == 2
-    assert M(FAKE, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 4, None) == 6
-    assert M(FAKE + 4, None, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
-    assert M(FAKE, FAKE + 2, 1, 1, 1, 64, 64, 64, 0, FAKE, 1 << 20, None) == 4
+    assert M(None, None, 1, 1, 1, 64, 64, 64, FAKE, 1 << 20, None) == 1
+    assert M(FAKE, None, 1, 2, 3, 64, 64, 64, FAKE, 1 << 20, None) == 2
+    assert M(FAKE, None, 1, 1, 1, 64, 64, 64, FAKE, 4, None) == 6
+    assert M(FAKE + 4, None, 1, 1, 1, 64, 64, 64, FAKE, 1 << 20, None) == 4
+    assert M(FAKE, FAKE + 2, 1, 1, 1, 64, 64, 64, FAKE, 1 << 20, None) == 4
+    # the tuning forms take T and chunk_rows
+    PX = lib.da_decode_partial_ex
+    assert PX(FAKE, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 1, 384,
+              FAKE, 1 << 20, None) == 2
+    assert PX(FAKE, FAKE, FAKE, None, None, FAKE, 0.1, 1, 1, 1, 64, 64, 64, 0, 0,
+              FAKE, 1 << 20, None) == 2
+    MX = lib.da_decode_merge_ex
+    assert MX(FAKE, None, 1, 1, 1, 64, 64, 64, 1, 100, FAKE, 1 << 20, None) == 2
+    assert MX(FAKE, None, 1, 1, 1, 64, 64, 64, 4097, 0, FAKE, 1 << 20, None) == 2
+
+
+def test_workspace_reset_validation():
+    R = lib.da_decode_workspace_reset
+    nc = binding.workspace_counter_bytes(2, 8, 2, 1000, 128, 128)
+    assert R(None, 1 << 20, 2, 8, 2, 1000, 128, 128, None) == 1
+    assert R(FAKE, 1 << 20, 2, 3, 2, 1000, 128, 128, None) == 2
+    assert R(FAKE, 1 << 20, 2, 8, 2, 1000, 96, 128, None) == 3
+    assert R(FAKE, nc - 16, 2, 8, 2, 1000, 128, 128, None) == 6
+    assert R(FAKE + 4, 1 << 20, 2, 8, 2, 1000, 128, 128, None) == 4
 
 
 def test_step_validation():
     S = lib.da_decode_step
-    args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 1, 1, 64, 64, 64, 0,
+    args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 1, 1, 64, 64, 64,
             FAKE, 1 << 20, None]
     for pos in (0, 1, 2, 3, 4, 5, 7):
         a = list(args); a[pos] = None
@@ -143,7 +217,7 @@ def test_step_validation():
     for pos in (3, 4, 7):
         a = list(args); a[pos] = FAKE + 4
         assert S(*a) == 4, pos
-    a = list(args); a[16] = 8
+    a = list(args); a[15] = 8
     assert S(*a) == 6
     a = list(args); a[6] = float("nan")
     assert S(*a) == 5
@@ -155,19 +229,19 @@ def test_step_validation():
 
 def test_multi_row_validation():
     D = lib.da_decode_multi
-    base = [FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, 0, FAKE, 1 << 20, None]
+    base = [FAKE, FAKE, FAKE, FAKE, 0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, FAKE, 1 << 20, None]
     for pos in (0, 1, 2, 3, 5):
         a = list(base); a[pos] = None
         assert D(*a) == 1, pos
     for T in (0, -1, 4097):
         a = list(base); a[12] = T
         assert D(*a) == 2, T
-    a = list(base); a[15] = 16
+    a = list(base); a[14] = 16
     assert D(*a) == 6
     a = list(base); a[5] = FAKE + 4
     assert D(*a) == 4
     S = lib.da_decode_multi_step
-    sb = [FAKE] * 6 + [0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, 0, FAKE, 1 << 20, None]
+    sb = [FAKE] * 6 + [0.1, FAKE, 1, 2, 1, 64, 64, 64, 4, FAKE, 1 << 20, None]
     for pos in (3, 4, 5, 7):
         a = list(sb); a[pos] = None
         assert S(*a) == 1, pos
