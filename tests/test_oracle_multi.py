@@ -107,6 +107,41 @@ def test_equals_t_single_steps_bit_for_bit():
     assert np.array_equal(seq, chunk)
 
 
+def test_near_capacity_the_two_multi_row_forms_differ_as_documented():
+    """T single steps (what the fused multi-row step computes) and append_rows
+    + decode_multi coincide only while every row fits.  With len = n_max - 2
+    and T = 4, single step r attends min(len + r + 1, n_max) rows, the
+    multi-row decode's row r attends n_max - T + r + 1 rows (the cache's last
+    T positions); a full cache (len = n_max) appends nothing and both then
+    attend n_max - T + r + 1 ... n_max rows differently again."""
+    B, h_q, h_kv, n_max, d, T = 2, 4, 2, 40, 8, 4
+    shape = workloads.custom("near_cap_o", B=B, h_q=h_q, h_kv=h_kv, d_k=d, d_v=d,
+                             n_max=n_max)
+    inp = workloads.make(shape, seed=3, lens=np.array([n_max - 2, n_max], np.int32))
+    kn, vn, q = _rand(20, (B, h_kv, T, d)), _rand(21, (B, h_kv, T, d)), _rand(22, (B, h_q, T, d))
+    K1, V1, l1 = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    seq = np.zeros((B, h_q, T, d))
+    for r in range(T):
+        oracle.append(K1, V1, np.ascontiguousarray(kn[:, :, r]),
+                      np.ascontiguousarray(vn[:, :, r]), l1)
+        seq[:, :, r] = oracle.decode(np.ascontiguousarray(q[:, :, r]), K1, V1, l1, 0.25)
+    K2, V2, l2 = inp.K.copy(), inp.V.copy(), inp.lens.copy()
+    oracle.append_rows(K2, V2, kn, vn, l2)
+    multi = oracle.decode_multi(q, K2, V2, l2, 0.25)
+    assert l1.tolist() == l2.tolist() == [n_max, n_max]
+    assert np.array_equal(K1.view(np.uint32), K2.view(np.uint32))
+    for r in range(T):
+        qr = np.ascontiguousarray(q[:, :, r])
+        seq_rows = np.minimum(inp.lens + r + 1, n_max).astype(np.int32)
+        multi_rows = np.full(B, n_max - T + r + 1, np.int32)
+        assert np.array_equal(seq[:, :, r], oracle.decode(qr, K1, V1, seq_rows, 0.25))
+        assert np.array_equal(multi[:, :, r], oracle.decode(qr, K1, V1, multi_rows, 0.25))
+    # the rows whose visibility differs give different outputs
+    assert not np.allclose(seq[0, :, 0], multi[0, :, 0])      # n_max-1 vs n_max-3 rows
+    assert np.array_equal(seq[0, :, 3], multi[0, :, 3])       # both see the whole cache
+    assert not np.allclose(seq[1, :, 0], multi[1, :, 0])      # full cache: n_max vs n_max-3
+
+
 def test_one_row_is_the_single_query_decode():
     q = _rand(10, (2, 4, 1, 8))
     K = _rand(11, (2, 2, 30, 8))
