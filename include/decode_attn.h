@@ -267,6 +267,27 @@ da_status da_kv_append_rows(float *K, float *V, const float *k_new,
                             int n_max, int d_k, int d_v, int T, void *stream);
 
 /*
+ * da_decode_attn without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): same arguments minus the workspace,
+ * same results, same validation.  The workspace is a fixed 64 MiB array in
+ * device memory that the library holds on every GPU it is loaded on, until
+ * the process ends; the call allocates nothing (no hipMalloc or allocating
+ * library routine).  Shapes whose da_decode_workspace_bytes() exceeds 64 MiB
+ * (67108864 bytes) are rejected with DA_ERR_WORKSPACE before anything is
+ * enqueued.  Each call first clears the array's counter region with a
+ * kernel.  All calls on one GPU share that GPU's array: calls that overlap
+ * in time on one GPU (concurrent streams, or several host threads) race and
+ * give wrong results; serialise them, or use da_decode_attn with separate
+ * workspaces.  DA_ERR_HIP also reports a failed lookup of the array.
+ */
+da_status da_decode_attn_noalloc(const float *q, const float *K,
+                                 const float *V, const int32_t *len,
+                                 float scale, float *out, int B, int h_q,
+                                 int h_kv, int n_max, int d_k, int d_v,
+                                 void *stream);
+
+/*
  * ---------------------------------------------------------------------------
  * Tuning and testing only.  The entry points above choose their own segment
  * size (the most rows a workgroup reads from its static range in one go,

@@ -11,7 +11,7 @@ built library; using the decode or append without it raises ImportError.
 from importlib import import_module
 
 _BINDING_NAMES = {
-    "decode_attn", "decode_step", "decode_partial", "decode_merge", "kv_append",
+    "decode_attn", "decode_attn_noalloc", "decode_step", "decode_partial", "decode_merge", "kv_append",
     "decode_multi", "decode_multi_step", "kv_append_rows", "alloc_multi_workspace",
     "chunk_rows", "workspace_bytes", "workspace_counter_bytes", "workspace_reset",
     "alloc_workspace", "DecodeAttnError",

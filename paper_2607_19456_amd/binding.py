@@ -38,6 +38,7 @@ SIGNATURES = {
     "da_decode_multi_step": (_ci, [_vp] * 6 + [_cf, _vp] + [_ci] * 7 + [_vp, _sz, _vp]),
     "da_kv_append": (_ci, [_vp] * 5 + [_ci] * 5 + [_vp]),
     "da_kv_append_rows": (_ci, [_vp] * 5 + [_ci] * 6 + [_vp]),
+    "da_decode_attn_noalloc": (_ci, [_vp, _vp, _vp, _vp, _cf, _vp] + [_ci] * 6 + [_vp]),
     # tuning and testing only (explicit segment size)
     "da_decode_chunk_rows": (_ci, [_ci] * 6),
     "da_decode_workspace_bytes_ex": (_sz, [_ci] * 7),
@@ -165,6 +166,22 @@ def decode_attn(q, K, V, lens, scale: float, out=None, workspace=None,
             *args, 1, int(chunk_rows), wp, wn, _stream(stream)))
     else:
         _check("da_decode_attn", _lib.da_decode_attn(*args, wp, wn, _stream(stream)))
+    return out
+
+
+NOALLOC_MAX_WORKSPACE_BYTES = 64 << 20
+
+
+def decode_attn_noalloc(q, K, V, lens, scale: float, out, stream=None) -> torch.Tensor:
+    """decode_attn on the library's own static workspace (no allocation by
+    the library; ``out`` is the caller's).  Calls on one GPU must not
+    overlap in time."""
+    B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
+    _check("da_decode_attn_noalloc", _lib.da_decode_attn_noalloc(
+        _dev(q, "q", torch.float32), _dev(K, "K", torch.float32),
+        _dev(V, "V", torch.float32), _dev(lens, "len", torch.int32),
+        float(scale), _dev(out, "out", torch.float32), B, h_q, h_kv, n_max, d_k, d_v,
+        _stream(stream)))
     return out
 
 

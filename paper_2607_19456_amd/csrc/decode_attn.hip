@@ -1511,6 +1511,31 @@ da_status clear_words(void* p, size_t bytes, hipStream_t s) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Library-owned workspace for da_decode_attn_noalloc: a fixed array in device
+// memory, one copy per GPU the library is loaded on, held until the process
+// ends.  On the host, `scratch` names a host-side stand-in, never device
+// memory: its device address is looked up per device (hipGetSymbolAddress)
+// and only that address is passed to kernels.
+// ---------------------------------------------------------------------------
+static constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+static std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's `scratch`, looked up on the first call on
+// the device (with the device current) and kept; nullptr on a HIP error.
+static void* scratch_address(int dev) {
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  g_scratch_ptr[dev].store(p, std::memory_order_release);
+  return p;
+}
+
 extern "C" {
 
 const char* da_status_string(da_status status) {
@@ -1669,6 +1694,36 @@ da_status da_decode_merge_ex(float* out, int32_t* len, int B, int h_q, int h_kv,
                              size_t workspace_bytes, void* stream) {
   return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, T, chunk_rows, workspace,
                     workspace_bytes, stream);
+}
+
+// --- no allocation: the library's own static workspace ----------------------
+
+da_status da_decode_attn_noalloc(const float* q, const float* K, const float* V,
+                                 const int32_t* len, float scale, float* out, int B, int h_q,
+                                 int h_kv, int n_max, int d_k, int d_v, void* stream) {
+  if (!q || !K || !V || !len || !out) return DA_ERR_NULL;
+  Plan pl;
+  da_status st = make_plan(B, h_q, h_kv, n_max, d_k, d_v, 0, kMaxResident, &pl);
+  if (st != DA_OK) return st;
+  if (pl.bytes > kScratchBytes) return DA_ERR_WORKSPACE;
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(len, 4) ||
+      !aligned(out, 16))
+    return DA_ERR_ALIGN;
+  if (!std::isfinite(scale)) return DA_ERR_SCALE;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return DA_ERR_HIP;
+  }
+  void* ws = scratch_address(dev);
+  if (!ws) return DA_ERR_HIP;
+  // The array keeps the last call's contents, possibly of other shapes: the
+  // counter region of these shapes starts from zero.
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = clear_words(ws, pl.counter_bytes, s);
+  if (st != DA_OK) return st;
+  return da_decode_multi_ex(q, K, V, len, scale, out, B, h_q, h_kv, n_max, d_k, d_v, 1, 0, ws,
+                            kScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -275,6 +275,29 @@ def test_append_validation(args, status):
     assert lib.da_kv_append(*args, None) == status
 
 
+def test_noalloc_validation():
+    """The no-allocation decode validates like da_decode_attn and rejects
+    shapes whose workspace exceeds its 64 MiB array, all on the host."""
+    N = lib.da_decode_attn_noalloc
+    args = [FAKE, FAKE, FAKE, FAKE, 0.125, FAKE, 4, 64, 8, 131072, 128, 128, None]
+    for pos in (0, 1, 2, 3, 5):
+        a = list(args); a[pos] = None
+        assert N(*a) == 1, pos
+    a = list(args); a[7] = 7
+    assert N(*a) == 2
+    a = list(args); a[10] = 96
+    assert N(*a) == 3
+    a = list(args); a[0] = FAKE + 4
+    assert N(*a) == 4
+    a = list(args); a[4] = float("nan")
+    assert N(*a) == 5
+    big = [FAKE, FAKE, FAKE, FAKE, 0.125, FAKE, 128, 32, 8, 32768, 128, 128, None]
+    assert binding.workspace_bytes(*big[6:12]) > binding.NOALLOC_MAX_WORKSPACE_BYTES
+    assert N(*big) == 6
+    assert binding.workspace_bytes(4, 64, 8, 131072, 128, 128) <= \
+        binding.NOALLOC_MAX_WORKSPACE_BYTES
+
+
 def test_binding_fails_loudly_without_the_library(tmp_path):
     env = dict(os.environ, DECODE_ATTN_LIB=str(tmp_path / "missing.so"))
     code = ("import paper_2607_19456_amd as p\n"
