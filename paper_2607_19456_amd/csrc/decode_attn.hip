@@ -21,8 +21,11 @@
 //   A resident grid of 256-thread workgroups (4 waves) shares the slabs' rows:
 //   most of each slab in ranges fixed in advance, proportional to the
 //   lengths, the rest in small units handed out by per-slab counters; a
-//   workgroup's waves take each segment's 16-row tiles round-robin.  Each
-//   tile is two dense products on the matrix cores
+//   workgroup's four waves share each 64-row turn of a segment, 16 rows
+//   each (with one column block the waves' rows interleave in groups of
+//   256/d rows, so the four waves' loads of one instruction cover 4 KB of
+//   consecutive rows; see "Row-pair layout").  Each tile is two dense
+//   products on the matrix cores
 //   (v_mfma_f32_16x16x4_f32, fp32 in and out):
 //     scores  S[16 rows x 16 heads] = K_tile[16 x d_k] . Q^T[d_k x 16]
 //     update  O^T[d_v x 16 heads]  += V_tile^T[d_v x 16] . P[16 x 16 heads]
@@ -87,8 +90,13 @@ constexpr int kMaxResident = 256;
 // two-tile ring (the W = 2 instances): two co-resident workgroups overlap
 // one's start and drain with the other's streaming, 3.5-7.5 % faster on
 // short caches (n <= 768) of many slabs.
+// Tiles in the ring of the persistent (one wave per SIMD) instances; the
+// host's scheduling unit is one turn of it.
+__host__ __device__ constexpr int ring_tiles(int nb, int dk, int dv) {
+  return dk + dv > 256 ? 2 : (nb == 2 ? 4 : 3);
+}
 template <int NB, int DK, int DV>
-constexpr int kRing = DK + DV > 256 ? 2 : (NB == 2 ? 4 : 3);
+constexpr int kRing = ring_tiles(NB, DK, DV);
 // q of the visit's heads (the B operand of the score products) is held in
 // registers for the whole visit where they fit (NB * d_k / 4 per lane, one
 // wave per SIMD), else re-read from LDS for every tile.  Two column blocks
@@ -253,6 +261,12 @@ struct RowSource {
   int fast_end;
   uint32_t k_lane;          // byte offset of lane (i,k) in a K tile: i*d_k + 4k floats
   uint32_t v_lane;          // byte offset of lane (i,k) in a V tile: 4k*d_v + 4i floats
+  // Row-pair layout only (see below).
+  int wave;                 // this wave's index in the workgroup
+  int first_off, max_off;   // offsets of the wave's first and last tile row from its turn
+  uint32_t kw_lane;         // LDS byte offset this lane writes K to (plus a per-load constant)
+  uint32_t kr_lane;         // LDS byte offset this lane reads K from (plus 64 bytes per t)
+  int rowoff[4];            // offset from the turn of the row score component r stands for
 };
 
 // ROWS: a fused append may add several rows (multi-row steps); otherwise at
@@ -302,6 +316,246 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
 #pragma unroll
     for (int c = 0; c < DV / 64; ++c) T.v[rho][c] = load4_stream(vp + 64 * c + 4 * i);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Row-pair layout (one column block, one wave per SIMD).  Each 16-byte load
+// instruction of a wave reads 1 KB of consecutive cache rows -- 256/d rows of
+// a d-wide tensor (2 rows at d = 128) -- instead of 64 bytes from each of 16
+// rows, so that every instruction covers whole 128-byte lines of one
+// contiguous run.  The MFMA operands need 16 rows spread over the lanes, so:
+//   V: two (d = 128) or four (d = 256) loaded registers are regrouped with
+//      v_permlane16_swap / v_permlane32_swap into the A-operand layout of the
+//      update product (lane (i,k): one row per lane-row k, dims 4i..4i+3 of a
+//      64-dim block); at d = 64 a load already is that layout.  This fixes
+//      which tile row each score row must be: update group rho takes tile rows
+//      upd_row(rho, k), k = 0..3, so score row 4k + rho is tile row
+//      upd_row(rho, k).
+//   K: written to a wave-private LDS tile whose slots are the score rows (slot
+//      4k + rho holds tile row upd_row(rho, k)), then read back in the A-operand
+//      layout of the score product (lane (i,k) reads slot i, dims
+//      16t + 4k..+3).  A slot is d_k + 4 floats wide, so the 8 lanes of a
+//      128-bit LDS access hit 8 different bank groups on both sides.
+// With kAdjacent the four waves of a workgroup read neighbouring row groups:
+// a wave's tile rows interleave with the other waves' across the 64-row turn
+// (4 KB contiguous per workgroup and load instruction) instead of being 16
+// consecutive rows.
+// ---------------------------------------------------------------------------
+template <int NB, int W>
+constexpr bool kPairs = NB == 1 && W == 1;
+// (K and V must cover the same rows per load for the interleaved order.)
+template <int DK, int DV>
+constexpr bool kAdjacent = DK == DV;
+
+// Offset of tile row q (0..15) of wave w from the first row of its turn; rpl
+// rows per load instruction.
+template <int RPL, bool ADJ>
+__device__ __forceinline__ int tile_row_off(int q, int w) {
+  if constexpr (ADJ) return 4 * RPL * (q / RPL) + RPL * w + q % RPL;
+  else return 16 * w + q;
+}
+
+// Tile row of lane-row k in update group rho (the row order the V regrouping
+// produces).
+template <int DV>
+__host__ __device__ constexpr int upd_row(int rho, int k) {
+  return DV == 128 ? 4 * rho + 2 * (k & 1) + (k >> 1) : 4 * rho + k;
+}
+
+// LDS slot (= score row) of tile row q: the inverse of upd_row.
+template <int DV>
+__host__ __device__ constexpr int slot_of_row(int q) {
+  return DV == 128 ? 4 * (((q >> 1) & 1) + 2 * (q & 1)) + (q >> 2) : 4 * (q & 3) + (q >> 2);
+}
+
+// Bytes per LDS slot of the K tile.
+template <int DK>
+constexpr int kKSlot = 4 * DK + 16;
+
+__device__ __forceinline__ void swap16(f4& a, f4& b) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a[e]), __float_as_uint(b[e]),
+                                                    false, false);
+    a[e] = __uint_as_float(r[0]);
+    b[e] = __uint_as_float(r[1]);
+  }
+}
+
+__device__ __forceinline__ void swap32(f4& a, f4& b) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a[e]), __float_as_uint(b[e]),
+                                                    false, false);
+    a[e] = __uint_as_float(r[0]);
+    b[e] = __uint_as_float(r[1]);
+  }
+}
+
+// Per-lane constants of the row-pair layout for wave w, lane (i, k).
+template <int DK, int DV>
+__device__ __forceinline__ void pair_lane_setup(RowSource& src, int w, int i, int k) {
+  constexpr bool ADJ = kAdjacent<DK, DV>;
+  constexpr int RK = 256 / DK, RV = 256 / DV;
+  const int lane = i + 16 * k;
+  src.wave = w;
+  // (for ADJ, d_k = d_v: one rows-per-load for both)
+  src.first_off = tile_row_off<RV, ADJ>(0, w);
+  src.max_off = tile_row_off<RV, ADJ>(15, w);
+  src.k_lane = (uint32_t)(tile_row_off<RK, ADJ>(0, w) * DK * 4 + 16 * lane);
+  src.v_lane = (uint32_t)(tile_row_off<RV, ADJ>(0, w) * DV * 4 + 16 * lane);
+  const int jk = lane / (DK / 4), ck = lane % (DK / 4);
+  src.kw_lane = (uint32_t)(slot_of_row<DV>(jk) * kKSlot<DK> + 16 * ck);
+  src.kr_lane = (uint32_t)(i * kKSlot<DK> + 16 * k);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) src.rowoff[r] = tile_row_off<RV, ADJ>(upd_row<DV>(r, k), w);
+}
+
+// Loads of one tile in the row-pair layout: load m of K covers tile rows
+// RK*m .. RK*m+RK-1 (lane: row RK*m + lane/(d_k/4), 16-byte piece lane %
+// (d_k/4)), likewise V.  row0 = the turn's first row + first_off.
+template <int DK, int DV, int NB, bool ROWS>
+__device__ __forceinline__ void load_tile_pairs(Tile<DK, DV, NB>& T, const RowSource& src,
+                                                int row0, int last_row, int lane) {
+  constexpr bool ADJ = kAdjacent<DK, DV>;
+  constexpr int RK = 256 / DK, RV = 256 / DV;
+  constexpr int kStep = ADJ ? 4096 : 1024;            // bytes between a wave's loads
+  const int tb = row0 - src.first_off;
+  if (tb + src.max_off < src.fast_end) {
+    const char* kb = reinterpret_cast<const char*>(src.Ks + (int64_t)tb * DK) + src.k_lane;
+    const char* vb = reinterpret_cast<const char*>(src.Vs + (int64_t)tb * DV) + src.v_lane;
+#pragma unroll
+    for (int m = 0; m < DK / 16; ++m)
+      T.k[m] = load4_stream(reinterpret_cast<const float*>(kb + m * kStep));
+#pragma unroll
+    for (int m = 0; m < DV / 16; ++m)
+      T.v[m / (DV / 64)][m % (DV / 64)] =
+          load4_stream(reinterpret_cast<const float*>(vb + m * kStep));
+    return;
+  }
+  // Rows past the end clamp to the last row (and to row 0 for the dummy
+  // loads past a visit's end); appended rows come from k_new / v_new.
+  auto source = [&](const float* base, const float* nbase, int D, int row) -> const float* {
+    row = max(0, min(row, last_row));
+    if constexpr (ROWS) {
+      if ((unsigned)(row - src.new_lo) < (unsigned)src.new_cnt)
+        return nbase + (int64_t)(row - src.new_lo) * D;
+    } else {
+      if (row == src.new_row) return nbase;
+    }
+    return base + (int64_t)row * D;
+  };
+  const int jk = lane / (DK / 4), ck = lane % (DK / 4);
+#pragma unroll
+  for (int m = 0; m < DK / 16; ++m) {
+    const int row = tb + tile_row_off<RK, ADJ>(RK * m + jk, src.wave);
+    T.k[m] = load4_stream(source(src.Ks, src.k_new_rows, DK, row) + 4 * ck);
+  }
+  const int jv = lane / (DV / 4), cv = lane % (DV / 4);
+#pragma unroll
+  for (int m = 0; m < DV / 16; ++m) {
+    const int row = tb + tile_row_off<RV, ADJ>(RV * m + jv, src.wave);
+    T.v[m / (DV / 64)][m % (DV / 64)] = load4_stream(source(src.Vs, src.v_new_rows, DV, row) + 4 * cv);
+  }
+}
+
+// One tile in the row-pair layout, one column block: K through the wave's LDS
+// slots into the score operand layout, V regrouped into the update operand
+// layout, then the same products and online softmax as process_tile.
+template <int DK, int DV, int NB, bool CAUSAL, bool PINQ>
+__device__ __forceinline__ void process_tile_pairs(const Tile<DK, DV, NB>& T, int row0,
+                                                   const int (&lim)[NB], const RowSource& src,
+                                                   int lane, char* __restrict__ wk,
+                                                   const f4 (*__restrict__ sh_q)[DK / 16][kWave],
+                                                   const f4 (&qr)[NB][DK / 16],
+                                                   float (&m_run)[NB], float (&l_run)[NB],
+                                                   f4 (&acc)[NB][DV / 64][4]) {
+  static_assert(NB == 1, "row-pair layout: one column block");
+  constexpr int RK = 256 / DK;
+  if constexpr (!PINQ) asm volatile("" ::: "memory");
+  // K: tile rows to their score-row slots, then the operand layout.
+#pragma unroll
+  for (int m = 0; m < DK / 16; ++m)
+    *reinterpret_cast<f4*>(wk + src.kw_lane + slot_of_row<DV>(RK * m) * kKSlot<DK>) = T.k[m];
+  __builtin_amdgcn_wave_barrier();
+  f4 kt[DK / 16];
+#pragma unroll
+  for (int t = 0; t < DK / 16; ++t)
+    kt[t] = *reinterpret_cast<const f4*>(wk + src.kr_lane + 64 * t);
+  __builtin_amdgcn_wave_barrier();
+  // V: the update operand of group rho, block c.
+  f4 va[4][DV / 64];
+#pragma unroll
+  for (int rho = 0; rho < 4; ++rho)
+#pragma unroll
+    for (int c = 0; c < DV / 64; ++c) va[rho][c] = T.v[rho][c];
+  if constexpr (DV == 128) {
+#pragma unroll
+    for (int rho = 0; rho < 4; ++rho) swap16(va[rho][0], va[rho][1]);
+  } else if constexpr (DV == 256) {
+#pragma unroll
+    for (int rho = 0; rho < 4; ++rho) {
+      swap32(va[rho][0], va[rho][2]);
+      swap32(va[rho][1], va[rho][3]);
+      swap16(va[rho][0], va[rho][1]);
+      swap16(va[rho][2], va[rho][3]);
+    }
+  }
+  auto Q = [&](int t) -> f4 {
+    if constexpr (PINQ) return qr[0][t];
+    else return sh_q[0][t][lane];
+  };
+  f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+  for (int t = 0; t < DK / 16; t += 2) {
+    const f4 q0 = Q(t), q1 = Q(t + 1);
+    s0 = mfma_16x16x4(kt[t].x, q0.x, s0);
+    s1 = mfma_16x16x4(kt[t + 1].x, q1.x, s1);
+    s0 = mfma_16x16x4(kt[t].y, q0.y, s0);
+    s1 = mfma_16x16x4(kt[t + 1].y, q1.y, s1);
+    s0 = mfma_16x16x4(kt[t].z, q0.z, s0);
+    s1 = mfma_16x16x4(kt[t + 1].z, q1.z, s1);
+    s0 = mfma_16x16x4(kt[t].w, q0.w, s0);
+    s1 = mfma_16x16x4(kt[t + 1].w, q1.w, s1);
+  }
+  f4 s = s0 + s1;
+  const int tb = row0 - src.first_off;
+  if (CAUSAL || tb + src.max_off > lim[0]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (tb + src.rowoff[r] > lim[0]) s[r] = -INFINITY;
+  }
+  const float tmax = max_over_row_groups(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
+  const bool bump = tmax > m_run[0] + kLazyMax;
+  if (__any(bump)) {
+    const float m_new = bump ? tmax : m_run[0];
+    float m_ref = m_new;
+    if constexpr (CAUSAL) m_ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run[0] - m_ref);
+    l_run[0] *= alpha;
+#pragma unroll
+    for (int c = 0; c < DV / 64; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[0][c][e] *= alpha;
+    m_run[0] = m_new;
+  }
+  float m_ref = m_run[0];
+  if constexpr (CAUSAL) m_ref = m_ref == -INFINITY ? 0.f : m_ref;
+  f4 pr;
+  pr[0] = fast_exp2(s[0] - m_ref);
+  pr[1] = fast_exp2(s[1] - m_ref);
+  pr[2] = fast_exp2(s[2] - m_ref);
+  pr[3] = fast_exp2(s[3] - m_ref);
+  l_run[0] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+#pragma unroll
+  for (int rho = 0; rho < 4; ++rho)
+#pragma unroll
+    for (int c = 0; c < DV / 64; ++c) {
+      acc[0][c][0] = mfma_16x16x4(va[rho][c].x, pr[rho], acc[0][c][0]);
+      acc[0][c][1] = mfma_16x16x4(va[rho][c].y, pr[rho], acc[0][c][1]);
+      acc[0][c][2] = mfma_16x16x4(va[rho][c].z, pr[rho], acc[0][c][2]);
+      acc[0][c][3] = mfma_16x16x4(va[rho][c].w, pr[rho], acc[0][c][3]);
+    }
 }
 
 // One 16-row tile for NB column blocks of query heads: scores on the matrix
@@ -669,6 +923,9 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
   __shared__ f4 sh_acc[kWaves - 1][NB][DV / 64][4][kWave];
   __shared__ float sh_m[kWaves - 1][NB][kWave];
   __shared__ float sh_l[kWaves - 1][NB][kWave];
+  // Row-pair layout: each wave's K tile, 16 slots of d_k + 4 floats.
+  constexpr bool PAIRS = kPairs<NB, W>;
+  __shared__ __align__(16) char sh_k[PAIRS ? kWaves : 1][PAIRS ? 16 * kKSlot<DK> : 16];
 
   // Fused append: the workgroups share the row copies -- rows len[b] + r of
   // every KV head <- k_new / v_new row r (those that fit), bit for bit.  The
@@ -871,6 +1128,8 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     src.v_new_rows = app ? v_new + slab * T * DV : nullptr;
     src.k_lane = (uint32_t)(i * DK + 4 * k) * sizeof(float);
     src.v_lane = (uint32_t)(4 * k * DV + 4 * i) * sizeof(float);
+    src.first_off = kTileRows * wave;
+    if constexpr (PAIRS) pair_lane_setup<DK, DV>(src, wave, i, k);
 
     // Last row each lane's column sees.  A causal column is query row
     // r = (its index in the KV head's group) mod T, at position pos0 + r:
@@ -924,9 +1183,10 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
       ns = dyn ? dyn_row(d0_used ? d1 : d0) : -1;
       ntpw = tpw_d;
     }
+    // First row of the wave's tile x of the stream (its smallest row).
     auto row_of = [&](int x) {
-      return x < ctpw ? cs + x * kRowsPerTurn + wave * kTileRows
-                      : (ns >= 0 ? ns + (x - ctpw) * kRowsPerTurn + wave * kTileRows : last_row);
+      return x < ctpw ? cs + x * kRowsPerTurn + src.first_off
+                      : (ns >= 0 ? ns + (x - ctpw) * kRowsPerTurn + src.first_off : last_row);
     };
     // B operand of the score product, staged in LDS in register order: entry
     // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
@@ -949,11 +1209,15 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     }
     constexpr int R = W == 2 ? 2 : kRing<NB, DK, DV>;
     Tile<DK, DV, NB> ring[R];
+    auto load = [&](Tile<DK, DV, NB>& T, int row0, int lr) {
+      if constexpr (PAIRS) load_tile_pairs<DK, DV, NB, CAUSAL>(T, src, row0, lr, lane);
+      else load_tile<DK, DV, NB, CAUSAL>(T, src, row0, lr, i, k);
+    };
     // (Unconditional, so that the wait for q counts only the q loads; a
     // visit without rows, which the schedule never opens, would read row 0.)
 #pragma unroll
     for (int p = 0; p < R - 1; ++p)
-      load_tile<DK, DV, NB, CAUSAL>(ring[p], src, cs >= 0 ? row_of(p) : 0, max(last_row, 0), i, k);
+      load(ring[p], cs >= 0 ? row_of(p) : 0, max(last_row, 0));
 #pragma unroll
     for (int u = 0; u < kQPerThread; ++u) {
       const int e = tid + u * kThreads;
@@ -1006,11 +1270,16 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
 #pragma unroll
           for (int p = 0; p < R; ++p) {
             const int r = row_of(t + p);
-            load_tile<DK, DV, NB, CAUSAL>(ring[(p + R - 1) % R], src, row_of(t + p + R - 1),
-                                          last_row, i, k);
-            if (r <= last_row)
-              process_tile<DK, DV, NB, CAUSAL, kPin>(ring[p], r, lim, k, lane, sh_q, qr, m_run,
-                                                     l_run, acc);
+            load(ring[(p + R - 1) % R], row_of(t + p + R - 1), last_row);
+            if (r <= last_row) {
+              if constexpr (PAIRS)
+                process_tile_pairs<DK, DV, NB, CAUSAL, kPin>(ring[p], r, lim, src, lane,
+                                                             sh_k[PAIRS ? wave : 0], sh_q, qr,
+                                                             m_run, l_run, acc);
+              else
+                process_tile<DK, DV, NB, CAUSAL, kPin>(ring[p], r, lim, k, lane, sh_q, qr, m_run,
+                                                       l_run, acc);
+            }
           }
           t += R;
           // A wave whose remaining tiles all lie past the slab's end (only
@@ -1311,7 +1580,7 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
                       ? kStaticDen : kStaticNum;
   // Scheduling units (static ranges and dynamic hand-outs) are one ring turn
   // of the four waves when there is a static share, else whole chunks.
-  const int ring = d_k + d_v > 256 ? 2 : (plan->blocks == 2 ? 4 : 3);
+  const int ring = ring_tiles(plan->blocks, d_k, d_v);
   plan->dyn_rows = plan->fnum > 0 ? ring * kWaves * kTileRows : chunk_rows;
   // Static slots: at most one per static unit of a slab plus one, and never
   // more than the workgroups.  Dynamic slots: every dynamic visit holds at
