@@ -119,16 +119,18 @@ def read_ceiling(a, b, stream, reps: int = 5):
 
 
 def host_cores() -> int:
+    """The CPUs this process may run on."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
         n = os.cpu_count() or 1
-    return max(1, min(16, n))
+    return max(1, n)
 
 
-def cpu_baseline(inp, budget_s: float, step_bytes, gpu_first=None):
+def cpu_baseline(inp, budget_s: float, step_bytes, gpu_first=None, threads=None):
     """Time the oracle (append + decode of every head, step after step) on
-    this host until about budget_s seconds of work are done.  With
+    this host until about budget_s seconds of work are done, with ``threads``
+    OpenMP threads (default: every CPU of this process's affinity).  With
     ``gpu_first`` (the GPU's output of the first step, every head), also
     return the max-abs-err between it and the oracle's first step."""
     import numpy as np
@@ -136,7 +138,7 @@ def cpu_baseline(inp, budget_s: float, step_bytes, gpu_first=None):
     import oracle
 
     s = inp.shape
-    threads = host_cores()
+    threads = threads or host_cores()
     hK, hV, hl = inp.K, inp.V, inp.lens.copy()
     done, elapsed, nbytes = 0, 0.0, 0
     steps = max(1, s.steps)
@@ -277,6 +279,9 @@ def main() -> int:
                          "(also len_lo, len_hi, rows; lengths default to n_max, less "
                          "steps*rows when there are steps)")
     ap.add_argument("--chunk-rows", type=int, default=0)
+    ap.add_argument("--settle-seconds", type=float, default=0.3,
+                    help="untimed repetitions of the step before the warm-up, so that "
+                         "the GPU runs at its steady clock (0: none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle sample (0: skip)")
     ap.add_argument("--conventional", action="store_true",
@@ -348,7 +353,7 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
-    def step(i, ev_a=None, ev_b=None):
+    def step(i, ev_a=None, ev_b=None, ev_c=None):
         # One step: the append fused into the decode's partial kernel, then
         # the merge (which also advances len) -- da_decode_step, with the
         # partial kernel bracketed by events.
@@ -381,7 +386,25 @@ def main() -> int:
             ev_b.record(st)
         binding.decode_merge(out, ws, s.B, s.h_q, s.h_kv, s.n_max, s.d_k, s.d_v,
                              ck, lens=dl if s.steps else None, stream=st)
+        if ev_c is not None:
+            ev_c.record(st)
 
+    # The GPU comes out of the idle input-drawing phase at a low clock and
+    # needs some tens of milliseconds of load to reach its steady clock (the
+    # first ~10 ms batch of a 64-step run measured 6 % slower than the ones
+    # after it).  Steady-state decoding keeps the GPU busy, so the step is
+    # first repeated, untimed, for --settle-seconds of wall time; then come
+    # the W warm-up steps and the K timed steps.
+    settled = 0
+    if args.settle_seconds > 0:
+        t_settle = time.perf_counter()
+        while time.perf_counter() - t_settle < args.settle_seconds:
+            for _ in range(8):
+                step(settled)
+                settled += 1
+            torch.cuda.synchronize()
+        dl.copy_(lens0)
+        log(f"settled the clock with {settled} untimed step(s)")
     log(f"warmup {args.warmup} step(s), chunk_rows={chunk}")
     for i in range(args.warmup):
         step(i)
@@ -402,6 +425,7 @@ def main() -> int:
 
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
+    merge_ms = None
     if args.graph:
         # The timed steps as one graph (the graph holds no memset, and the
         # workspace counters come back to zero after each step), replayed once
@@ -425,17 +449,20 @@ def main() -> int:
     else:
         ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
         ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        ev_c = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
         log(f"timing {args.steps} step(s)")
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
         start.record(stream)
         for i in range(args.steps):
-            step(i, ev_a[i], ev_b[i])
+            step(i, ev_a[i], ev_b[i], ev_c[i])
         end.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
         total_ms = start.elapsed_time(end)
         launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
+        if not (multi or direct):
+            merge_ms = [b.elapsed_time(c) for b, c in zip(ev_b, ev_c)]
 
     def step_bytes(lens, with_append=True):
         b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v, s.rows)
@@ -484,6 +511,7 @@ def main() -> int:
                      else "decode_partial + decode_merge"),
             "graph": bool(args.graph),
         },
+        "settle_steps_untimed": settled,
         "us_per_step": round(ms_per_step * 1e3, 2),
         "hbm_roofline_frac_step": round(value / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": int(alg_bytes / args.steps),
@@ -508,6 +536,40 @@ def main() -> int:
     }
     log(f"{ms_per_step * 1e3:.1f} us/step, {value:.0f} GB/s; partial "
         f"{launch_avg_ms * 1e3:.1f} us at {achieved:.0f} GB/s")
+
+    # The parts of a step, each timed with events on the same stream: the
+    # partial kernel (with the fused append) and the merge of the timed
+    # steps above, then the standalone append (da_kv_append, or
+    # da_kv_append_rows for several rows per step) over the same steps on
+    # its own.
+    comps = {"decode_partial_us": None, "decode_merge_us": None,
+             "kv_append_standalone_us": None, "kv_append_bytes_per_step": None}
+    if merge_ms is not None:
+        comps["decode_partial_us"] = round(launch_avg_ms * 1e3, 2)
+        comps["decode_merge_us"] = round(sum(merge_ms) / len(merge_ms) * 1e3, 2)
+    if s.steps:
+        dl.copy_(lens0)
+        torch.cuda.synchronize()
+        ea = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        eb = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        for i in range(args.steps):
+            t = i % nsteps_in
+            if t == 0 and i > 0:
+                dl.copy_(lens0)
+            ea[i].record(stream)
+            if multi:
+                binding.kv_append_rows(dK, dV, dkn[t], dvn[t], dl, stream=stream)
+            else:
+                binding.kv_append(dK, dV, dkn[t], dvn[t], dl, stream=stream)
+            eb[i].record(stream)
+        torch.cuda.synchronize()
+        comps["kv_append_standalone_us"] = round(
+            sum(a.elapsed_time(b) for a, b in zip(ea, eb)) / args.steps * 1e3, 2)
+        comps["kv_append_bytes_per_step"] = traffic.batch_append_bytes(
+            s.B, s.h_kv, s.d_k, s.d_v, s.rows)
+        dl.copy_(lens0)
+        log(f"standalone append: {comps['kv_append_standalone_us']} us per step")
+    result["step_components"] = comps
 
     # The machine's practical read ceiling on the same K and V allocations:
     # a plain non-temporal streaming read of every byte (not the decode).
@@ -545,6 +607,12 @@ def main() -> int:
         # the oracle replays the workload from its initial state
         result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, step_bytes, first_out)
         result["max_abs_err_vs_oracle"] = result["cpu_baseline"]["max_abs_err_first_step"]
+        if s.name in ("mha1_d64_n128", "gqa32x8_b16_d128_n8192"):
+            # the small and the GQA-4 single decode also on one thread
+            log("cpu_baseline: the oracle on one thread")
+            one = cpu_baseline(inp, min(args.cpu_seconds, 10.0), step_bytes, None, threads=1)
+            result["cpu_baseline"]["one_thread"] = {
+                k: one[k] for k in ("value", "unit", "cores", "sample", "seconds_per_step")}
         log(f"max-abs-err of the first step vs the oracle: {result['max_abs_err_vs_oracle']:.3e}")
     else:
         result["cpu_baseline"] = None

@@ -270,8 +270,9 @@ struct RowSource {
 };
 
 // ROWS: a fused append may add several rows (multi-row steps); otherwise at
-// most one, which keeps the redirect a single comparison.
-template <int DK, int DV, int NB, bool ROWS>
+// most one, which keeps the redirect a single comparison.  APP = false: no
+// fused append can occur (the direct form), no redirect at all.
+template <int DK, int DV, int NB, bool ROWS, bool APP = true>
 __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& src,
                                           int row0, int last_row, int i, int k) {
   if (row0 + kTileRows <= src.fast_end) {
@@ -292,10 +293,15 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
     return;
   }
   // The slab's last tile(s): rows past the end clamp to the last row, and
-  // the rows a fused append adds come from k_new / v_new.
+  // the rows a fused append adds come from k_new / v_new.  (The lane indices
+  // are made opaque here so that this rarely taken path's per-lane addresses
+  // are formed inside it, not hoisted out of the tile loop into registers.)
+  asm volatile("" : "+v"(i), "+v"(k));
   const int rk = min(row0 + i, last_row);
   const float* kp;
-  if constexpr (ROWS)
+  if constexpr (!APP)
+    kp = src.Ks + (int64_t)rk * DK;
+  else if constexpr (ROWS)
     kp = (unsigned)(rk - src.new_lo) < (unsigned)src.new_cnt
              ? src.k_new_rows + (rk - src.new_lo) * DK
              : src.Ks + (int64_t)rk * DK;
@@ -307,7 +313,9 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
   for (int rho = 0; rho < 4; ++rho) {
     const int rv = min(row0 + 4 * k + rho, last_row);
     const float* vp;
-    if constexpr (ROWS)
+    if constexpr (!APP)
+      vp = src.Vs + (int64_t)rv * DV;
+    else if constexpr (ROWS)
       vp = (unsigned)(rv - src.new_lo) < (unsigned)src.new_cnt
                ? src.v_new_rows + (rv - src.new_lo) * DV
                : src.Vs + (int64_t)rv * DV;
@@ -663,22 +671,22 @@ __device__ __forceinline__ void process_tile(const Tile<DK, DV, NB>& T, int row0
   }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    f4 qb[DK / 16];
-#pragma unroll
-    for (int t = 0; t < DK / 16; ++t) qb[t] = Q(nb, t);
     // Step I: s[row 4k+r][head i] for the tile's 16 rows (two independent
-    // accumulation chains over the d_k/4 steps, added at the end).
+    // accumulation chains over the d_k/4 steps, added at the end).  q is
+    // fetched pair by pair (from LDS unless pinned), so at two waves per SIMD
+    // only four of its registers are live at a time.
     f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < DK / 16; t += 2) {
-      s0 = mfma_16x16x4(T.k[t].x, qb[t].x, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].x, qb[t + 1].x, s1);
-      s0 = mfma_16x16x4(T.k[t].y, qb[t].y, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].y, qb[t + 1].y, s1);
-      s0 = mfma_16x16x4(T.k[t].z, qb[t].z, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].z, qb[t + 1].z, s1);
-      s0 = mfma_16x16x4(T.k[t].w, qb[t].w, s0);
-      s1 = mfma_16x16x4(T.k[t + 1].w, qb[t + 1].w, s1);
+      const f4 qa = Q(nb, t), qc = Q(nb, t + 1);
+      s0 = mfma_16x16x4(T.k[t].x, qa.x, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].x, qc.x, s1);
+      s0 = mfma_16x16x4(T.k[t].y, qa.y, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].y, qc.y, s1);
+      s0 = mfma_16x16x4(T.k[t].z, qa.z, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].z, qc.z, s1);
+      s0 = mfma_16x16x4(T.k[t].w, qa.w, s0);
+      s1 = mfma_16x16x4(T.k[t + 1].w, qc.w, s1);
     }
     f4 s = s0 + s1;
     // Rows past the last row this lane's column sees take no weight (only a
@@ -1211,7 +1219,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     Tile<DK, DV, NB> ring[R];
     auto load = [&](Tile<DK, DV, NB>& T, int row0, int lr) {
       if constexpr (PAIRS) load_tile_pairs<DK, DV, NB, CAUSAL>(T, src, row0, lr, lane);
-      else load_tile<DK, DV, NB, CAUSAL>(T, src, row0, lr, i, k);
+      else load_tile<DK, DV, NB, CAUSAL, W == 1>(T, src, row0, lr, i, k);
     };
     // (Unconditional, so that the wait for q counts only the q loads; a
     // visit without rows, which the schedule never opens, would read row 0.)
