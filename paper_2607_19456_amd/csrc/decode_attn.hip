@@ -1196,24 +1196,39 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
       return x < ctpw ? cs + x * kRowsPerTurn + src.first_off
                       : (ns >= 0 ? ns + (x - ctpw) * kRowsPerTurn + src.first_off : last_row);
     };
-    // B operand of the score product, staged in LDS in register order: entry
-    // [nb][t][lane (k, i)] = q of head nb*16+i at dims 16t+4k..+3, scaled into
-    // base-2 units (zero for the padding heads of a partial column block).
-    // The q loads go out first and the ring's first tiles right after them,
-    // so the tiles are in flight while q is written to LDS.
+    // B operand of the score product: lane (k, i) holds q of head nb*16+i at
+    // dims 16t+4k..+3, scaled into base-2 units (zero for the padding heads
+    // of a partial column block).  Where it is held in registers for the
+    // whole visit, every wave loads it straight into that layout; otherwise
+    // it is staged once in LDS in register order and re-read for every tile.
+    // Either way the q loads go out first and the ring's first tiles right
+    // after them, so the wait for q leaves the tiles in flight.
+    constexpr bool kPin = W == 1 && kPinQ<NB, DK>;
     constexpr int kQPerThread = NB * (DK / 16) * kWave / kThreads;
     static_assert(kQPerThread * kThreads == NB * (DK / 16) * kWave, "q staging");
-    f4 qv[kQPerThread];
+    f4 qr[NB][DK / 16];
+    f4 qv[kPin ? 1 : kQPerThread];
+    if constexpr (kPin) {
 #pragma unroll
-    for (int u = 0; u < kQPerThread; ++u) {
-      const int e = tid + u * kThreads;
-      const int ln = e % kWave;
-      const int t = (e / kWave) % (DK / 16);
-      const int nb = e / (kWave * (DK / 16));
-      const int hl = nb * kHeadsPerBlock + (ln & 15);
-      qv[u] = f4{0.f, 0.f, 0.f, 0.f};
-      if (hl < h_count)
-        qv[u] = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4));
+      for (int nb = 0; nb < NB; ++nb) {
+        const int hl = nb * kHeadsPerBlock + i;
+        const float* qh = q + ((int64_t)b * h_q + h_first + hl) * DK + 4 * k;
+#pragma unroll
+        for (int t = 0; t < DK / 16; ++t)
+          qr[nb][t] = hl < h_count ? load4(qh + 16 * t) : f4{0.f, 0.f, 0.f, 0.f};
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kQPerThread; ++u) {
+        const int e = tid + u * kThreads;
+        const int ln = e % kWave;
+        const int t = (e / kWave) % (DK / 16);
+        const int nb = e / (kWave * (DK / 16));
+        const int hl = nb * kHeadsPerBlock + (ln & 15);
+        qv[u] = f4{0.f, 0.f, 0.f, 0.f};
+        if (hl < h_count)
+          qv[u] = load4(q + ((int64_t)b * h_q + h_first + hl) * DK + 16 * t + 4 * (ln >> 4));
+      }
     }
     constexpr int R = W == 2 ? 2 : kRing<NB, DK, DV>;
     Tile<DK, DV, NB> ring[R];
@@ -1226,20 +1241,18 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
 #pragma unroll
     for (int p = 0; p < R - 1; ++p)
       load(ring[p], cs >= 0 ? row_of(p) : 0, max(last_row, 0));
-#pragma unroll
-    for (int u = 0; u < kQPerThread; ++u) {
-      const int e = tid + u * kThreads;
-      sh_q[e / (kWave * (DK / 16))][(e / kWave) % (DK / 16)][e % kWave] = qv[u] * qscale;
-    }
-    __syncthreads();
-    // (Two waves per SIMD leave no room for it.)
-    constexpr bool kPin = W == 1 && kPinQ<NB, DK>;
-    f4 qr[NB][DK / 16];
     if constexpr (kPin) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int t = 0; t < DK / 16; ++t) qr[nb][t] = sh_q[nb][t][lane];
+        for (int t = 0; t < DK / 16; ++t) qr[nb][t] *= qscale;
+    } else {
+#pragma unroll
+      for (int u = 0; u < kQPerThread; ++u) {
+        const int e = tid + u * kThreads;
+        sh_q[e / (kWave * (DK / 16))][(e / kWave) % (DK / 16)][e % kWave] = qv[u] * qscale;
+      }
+      __syncthreads();
     }
 
     // Running state per column block; lane (k, i) belongs to head i.
