@@ -345,6 +345,10 @@ def main() -> int:
     ck = args.chunk_rows
     chunk = ck or binding.chunk_rows(s.B, s.h_q * s.rows, s.h_kv, s.n_max, s.d_k, s.d_v)
     direct = not s.steps and not multi and chunk >= s.n_max
+    # A fused step on single-chunk slabs with one column block and
+    # d_k + d_v <= 256 is one launch as well (da_decode_step, direct form).
+    direct_step = (bool(s.steps) and not multi and not ck and chunk >= s.n_max
+                   and s.h_q // s.h_kv <= 16 and s.d_k + s.d_v <= 256)
     if multi:
         ws = binding.alloc_multi_workspace(dq[0], dK, dV, ck)
     else:
@@ -374,6 +378,12 @@ def main() -> int:
         if direct:
             binding.decode_attn(dq[t], dK, dV, dl, scale, out=out, workspace=ws,
                                 chunk_rows=ck, stream=st)
+            if ev_b is not None:
+                ev_b.record(st)
+            return
+        if direct_step:
+            binding.decode_step(dq[t], dK, dV, dkn[t], dvn[t], dl, scale, out=out,
+                                workspace=ws, stream=st)
             if ev_b is not None:
                 ev_b.record(st)
             return
@@ -468,7 +478,7 @@ def main() -> int:
         wall = time.perf_counter() - wall0
         total_ms = start.elapsed_time(end)
         launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
-        if not (multi or direct):
+        if not (multi or direct or direct_step):
             merge_ms = [b.elapsed_time(c) for b, c in zip(ev_b, ev_c)]
 
     def step_bytes(lens, with_append=True):
@@ -480,7 +490,7 @@ def main() -> int:
     alg_bytes = sum(step_bytes(l, bool(s.steps)) for l in step_lens)
     # The partial kernel of a step also writes the appended rows (Prop. 2).
     append_b = traffic.batch_append_bytes(s.B, s.h_kv, s.d_k, s.d_v, s.rows) if s.steps else 0
-    if multi or direct:   # the events hold the whole step
+    if multi or direct or direct_step:   # the events hold the whole step
         launch_bytes = [step_bytes(l, bool(s.steps)) for l in step_lens]
     else:
         launch_bytes = [traffic.batch_partial_bytes(l, s.h_q, s.h_kv, s.d_k, s.d_v) + append_b
@@ -514,6 +524,8 @@ def main() -> int:
             "step": ("da_decode_multi_step (T-row append fused, causal T-row decode)"
                      if multi else
                      "da_decode_attn (direct form: one launch, no merge)" if direct else
+                     "da_decode_step (direct form: append, decode and len advance in one "
+                     "launch)" if direct_step else
                      "decode_partial with fused kv_append + decode_merge" if s.steps
                      else "decode_partial + decode_merge"),
             "graph": bool(args.graph),
@@ -528,6 +540,7 @@ def main() -> int:
             "kernel": ("decode_partial_kernel + decode_merge_kernel (the whole step)"
                        if multi else
                        "decode_partial_kernel (direct form, the whole decode)" if direct
+                       else "decode_partial_kernel (direct form, the whole step)" if direct_step
                        else "decode_partial_kernel"),
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,
@@ -536,7 +549,7 @@ def main() -> int:
             "traffic": None if multi else counter_traffic(s.name),
             "avg_launch_us": round(launch_avg_ms * 1e3, 2),
             "timing": ("graph replay / steps" if args.graph
-                       else "HIP events around each step" if multi or direct
+                       else "HIP events around each step" if multi or direct or direct_step
                        else "HIP events around each partial launch"),
             "algorithmic_bytes_per_launch": int(sum(launch_bytes) / len(launch_bytes)),
         },

@@ -157,9 +157,13 @@ da_status da_decode_attn(const float *q, const float *K, const float *V,
  * (6)-(7) then (1)-(3), the order of one autoregressive step of the paper's
  * multi-step cache -- in two kernel launches instead of three: the partial
  * launch reads the new row of each KV head straight from k_new / v_new (and
- * writes it into the cache meanwhile), and the merge advances len.  Same
- * results, same argument rules as the two calls; k_new [B][h_kv][d_k] and
- * v_new [B][h_kv][d_v] must not overlap K / V.
+ * writes it into the cache meanwhile), and the merge advances len.  When
+ * every slab is short (n_max within one segment), h_q / h_kv <= 16 and
+ * d_k + d_v <= 256, the whole step is one launch: one workgroup per
+ * (b, KV head, head group) writes its output rows, and the last workgroup of
+ * each sequence to finish advances len[b].  Same results, same argument
+ * rules as the two calls; k_new [B][h_kv][d_k] and v_new [B][h_kv][d_v] must
+ * not overlap K / V.
  */
 da_status da_decode_step(const float *q, float *K, float *V,
                          const float *k_new, const float *v_new, int32_t *len,
@@ -224,8 +228,9 @@ da_status da_decode_multi(const float *q, const float *K, const float *V,
  * v_new [B][h_kv][T][d_v] appended at len[b] + r while the cache has room
  * (da_kv_append_rows), and query row r of q [B][h_q][T][d_k] attending rows
  * 0 .. min(len[b] + r, n_max - 1) of the grown cache (len[b] the value on
- * entry; nothing if len[b] < 0).  Two launches; len advances by the rows
- * that fit.  Workspace as da_decode_multi.
+ * entry; nothing if len[b] < 0).  Two launches (one under the conditions
+ * da_decode_step names, with h_q*T / h_kv for h_q / h_kv); len advances by
+ * the rows that fit.  Workspace as da_decode_multi.
  *
  * While every row fits (0 <= len[b] and len[b] + T <= n_max) this equals
  * da_kv_append_rows followed by da_decode_multi.  Near capacity the two

@@ -188,8 +188,9 @@ def decode_attn_noalloc(q, K, V, lens, scale: float, out, stream=None) -> torch.
 def decode_step(q, K, V, k_new, v_new, lens, scale: float, out=None, workspace=None,
                 chunk_rows: int = 0, stream=None) -> torch.Tensor:
     """kv_append(K, V, k_new, v_new, lens) then decode_attn(q, K, V, lens),
-    fused into two kernel launches (``chunk_rows`` != 0: the same two
-    launches through the tuning calls)."""
+    fused into two kernel launches, or one where every slab is a single
+    segment with h_q / h_kv <= 16 and d_k + d_v <= 256 (``chunk_rows`` != 0:
+    always two, through the tuning calls)."""
     B, h_q, h_kv, n_max, d_k, d_v = _shapes(q, K, V)
     _new_rows(k_new, v_new, B, h_kv, d_k, d_v)
     if out is None:

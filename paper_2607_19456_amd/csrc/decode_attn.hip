@@ -272,7 +272,7 @@ struct RowSource {
 // ROWS: a fused append may add several rows (multi-row steps); otherwise at
 // most one, which keeps the redirect a single comparison.  APP = false: no
 // fused append can occur (the direct form), no redirect at all.
-template <int DK, int DV, int NB, bool ROWS, bool APP = true>
+template <int DK, int DV, int NB, bool ROWS>
 __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& src,
                                           int row0, int last_row, int i, int k) {
   if (row0 + kTileRows <= src.fast_end) {
@@ -299,9 +299,7 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
   asm volatile("" : "+v"(i), "+v"(k));
   const int rk = min(row0 + i, last_row);
   const float* kp;
-  if constexpr (!APP)
-    kp = src.Ks + (int64_t)rk * DK;
-  else if constexpr (ROWS)
+  if constexpr (ROWS)
     kp = (unsigned)(rk - src.new_lo) < (unsigned)src.new_cnt
              ? src.k_new_rows + (rk - src.new_lo) * DK
              : src.Ks + (int64_t)rk * DK;
@@ -313,9 +311,7 @@ __device__ __forceinline__ void load_tile(Tile<DK, DV, NB>& T, const RowSource& 
   for (int rho = 0; rho < 4; ++rho) {
     const int rv = min(row0 + 4 * k + rho, last_row);
     const float* vp;
-    if constexpr (!APP)
-      vp = src.Vs + (int64_t)rv * DV;
-    else if constexpr (ROWS)
+    if constexpr (ROWS)
       vp = (unsigned)(rv - src.new_lo) < (unsigned)src.new_cnt
                ? src.v_new_rows + (rv - src.new_lo) * DV
                : src.Vs + (int64_t)rv * DV;
@@ -911,9 +907,13 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     const float* __restrict__ v_new, const int32_t* __restrict__ len, float qscale,
     int B, int h_q, int h_kv, int n_max, int T, int C, int Cd, int fnum, int head_groups, int J,
     int Jd, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
-    float* __restrict__ ws_acc, float* __restrict__ out_direct) {
+    float* __restrict__ ws_acc, float* __restrict__ out_direct, int32_t* len_bump) {
   // Whole-slab static ranges are planned for one column block only.
   if (NB == 2 && fnum > kStaticNum) fnum = kStaticNum;
+  // Two waves per SIMD serve only the direct form, which schedules nothing
+  // (out_direct is always set there): its scheduling code compiles away.
+  constexpr bool kDirect = W == 2;
+  if constexpr (kDirect) fnum = 0;
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
@@ -935,31 +935,30 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
   constexpr bool PAIRS = kPairs<NB, W>;
   __shared__ __align__(16) char sh_k[PAIRS ? kWaves : 1][PAIRS ? 16 * kKSlot<DK> : 16];
 
-  // Fused append: the workgroups share the row copies -- rows len[b] + r of
-  // every KV head <- k_new / v_new row r (those that fit), bit for bit.  The
-  // decode below never reads those rows from the cache (it takes them
-  // straight from k_new / v_new), so no ordering between the copies and the
-  // reads is needed; len[b] itself is only advanced by the merge, after every
-  // workgroup has read it.
-  if (app) {
-    constexpr int ck = DK / 4, cv = DV / 4;             // 16-byte chunks per row
-    for (int u = blockIdx.x; u < B * h_kv; u += gridDim.x) {
-      const int b = u / h_kv;
-      const int32_t t = len[b];
-      const int cnt = appended_rows(app, t, n_max, T);
-      for (int w = tid; w < cnt * (ck + cv); w += kThreads) {
-        const int r = w / (ck + cv);
-        const int x = w - r * (ck + cv);
-        const int64_t row = (int64_t)u * n_max + t + r;
-        const int64_t src = (int64_t)u * T + r;
-        if (x < ck)
-          reinterpret_cast<u4*>(K + row * DK)[x] = reinterpret_cast<const u4*>(k_new + src * DK)[x];
-        else
-          reinterpret_cast<u4*>(V + row * DV)[x - ck] =
-              reinterpret_cast<const u4*>(v_new + src * DV)[x - ck];
-      }
+  // Fused append: rows len[b] + r of KV head u = (b, g) <- k_new / v_new row
+  // r (those that fit), bit for bit.  The decode never reads those rows from
+  // the cache (it takes them straight from k_new / v_new), so no ordering
+  // between the copies and the reads is needed.  len[b] is advanced only
+  // once every workgroup has read it: by the merge, or in the direct form by
+  // the sequence's last workgroup (see the end of this kernel).
+  constexpr int ck = DK / 4, cv = DV / 4;               // 16-byte chunks per row
+  auto append_rows = [&](int u, int32_t t) {
+    const int cnt = appended_rows(app, t, n_max, T);
+    for (int w = tid; w < cnt * (ck + cv); w += kThreads) {
+      const int r = w / (ck + cv);
+      const int x = w - r * (ck + cv);
+      const int64_t row = (int64_t)u * n_max + t + r;
+      const int64_t src = (int64_t)u * T + r;
+      if (x < ck)
+        reinterpret_cast<u4*>(K + row * DK)[x] = reinterpret_cast<const u4*>(k_new + src * DK)[x];
+      else
+        reinterpret_cast<u4*>(V + row * DV)[x - ck] =
+            reinterpret_cast<const u4*>(v_new + src * DV)[x - ck];
     }
-  }
+  };
+  // Persistent form: the workgroups share the copies up front.
+  if (!kDirect && app)
+    for (int u = blockIdx.x; u < B * h_kv; u += gridDim.x) append_rows(u, len[u / h_kv]);
   int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
   // Direct form (out_direct set; every slab is a single chunk): workgroup s
   // owns slab s, takes its one chunk without searching and writes the output
@@ -988,8 +987,8 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     // no slab gets more than Jd of them.
     if (wave == 0) {
       int s = -1, j = -1, sr = 0, er = 0, d0 = -1, d1 = -1, dyn = 0;
-      int budget = (out_direct || fnum >= kStaticDen) ? 0 : S;
-      if (out_direct) {
+      int budget = (kDirect || out_direct || fnum >= kStaticDen) ? 0 : S;
+      if (kDirect || out_direct) {
         if (first) {
           s = blockIdx.x;
           j = 0;
@@ -1101,7 +1100,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     const int er = sh_ctl[3];
     const int d0 = sh_ctl[4];
     const int d1 = sh_ctl[5];
-    const bool dyn = sh_ctl[6] != 0;
+    const bool dyn = !kDirect && sh_ctl[6] != 0;
     if (s < 0) break;                                   // every slab is exhausted
     first = false;
 
@@ -1234,7 +1233,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     Tile<DK, DV, NB> ring[R];
     auto load = [&](Tile<DK, DV, NB>& T, int row0, int lr) {
       if constexpr (PAIRS) load_tile_pairs<DK, DV, NB, CAUSAL>(T, src, row0, lr, lane);
-      else load_tile<DK, DV, NB, CAUSAL, W == 1>(T, src, row0, lr, i, k);
+      else load_tile<DK, DV, NB, CAUSAL>(T, src, row0, lr, i, k);
     };
     // (Unconditional, so that the wait for q counts only the q loads; a
     // visit without rows, which the schedule never opens, would read row 0.)
@@ -1414,6 +1413,31 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     }
     // Wave 0 runs the next search; the barrier at its end keeps the other
     // waves from touching sh_q / sh_ctl before wave 0 is done here.
+  }
+
+  // Direct form of a fused append (the whole step in this one launch; two
+  // waves per SIMD, the only direct form that takes one): the
+  // first head group of each KV head copies its rows, then every workgroup
+  // of sequence b checks in on the sequence's counter (word 2 of the line of
+  // its first slab) once all its waves are done reading len[b].  The last to
+  // check in advances len[b] by the rows that fit and clears the counter for
+  // the next call.
+  if (kDirect && app) {
+    const int sd = (int)blockIdx.x;
+    const int b = sd / per_b;
+    const int rem = sd - b * per_b;
+    const int g = rem / head_groups;
+    const int32_t t = len[b];
+    if (rem - g * head_groups == 0) append_rows(b * h_kv + g, t);
+    // Every wave has read len[b] (its copies depend on it) before the check-in.
+    __syncthreads();
+    if (tid == 0 && len_bump) {
+      unsigned* arrivals = cnt + (size_t)b * per_b * kCounterStride + 2;
+      if (atomicAdd(arrivals, 1u) == (unsigned)per_b - 1u) {
+        *arrivals = 0u;
+        if (t >= 0 && t < n_max) len_bump[b] = t + min(T, n_max - t);
+      }
+    }
   }
 }
 
@@ -1654,20 +1678,28 @@ struct PartialArgs {
   int B, h_q, h_kv, n_max;   // h_q counts query rows: heads x T
   int T;                     // query rows per head (1: single-query decode)
   float* out_direct;         // set: single-chunk slabs, output written directly
+  int32_t* len_bump;         // direct form of a fused append: len, advanced in the kernel
 };
+
+// The direct form runs two waves per SIMD for one column block and
+// d_k + d_v <= 256; only that form takes a fused append.
+bool direct_two_waves(const Plan& pl, int d_k, int d_v) {
+  return pl.single_chunk && pl.blocks == 1 && d_k + d_v <= 256;
+}
 
 template <int DK, int DV, int NB, bool CAUSAL>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
   // The direct form runs one workgroup per slab; otherwise the resident grid.
   const unsigned grid = a.out_direct ? (unsigned)pl.slabs : (unsigned)pl.grid;
-  // The direct form schedules nothing: no static share.
+  // The direct form schedules nothing: no static share.  (The two-wave
+  // instances are the shapes direct_two_waves() names.)
   if constexpr (NB == 1 && DK + DV <= 256) {
     if (a.out_direct) {
       hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL, 2>), dim3(grid),
                          dim3(kThreads), 0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len,
                          a.qscale, a.B, a.h_q, a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.dyn_rows,
                          0, pl.head_groups, pl.J, pl.Jd, w.cnt, w.nvis, w.ml, w.acc,
-                         a.out_direct);
+                         a.out_direct, a.len_bump);
       return;
     }
   }
@@ -1675,7 +1707,7 @@ void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipSt
                      0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len, a.qscale, a.B, a.h_q,
                      a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.dyn_rows,
                      a.out_direct ? 0 : pl.fnum, pl.head_groups, pl.J, pl.Jd, w.cnt, w.nvis,
-                     w.ml, w.acc, a.out_direct);
+                     w.ml, w.acc, a.out_direct, a.len_bump);
 }
 
 template <int DK, int DV>
@@ -1729,11 +1761,15 @@ da_status partial_impl(const float* q, const float* K, const float* V, const flo
 
   const WsView w = view(pl, workspace);
   // K and V are written only when a fused append is asked for (k_new set).
-  // Direct form: only for a whole decode without a fused append (len is not
-  // advanced) whose slabs are single chunks.
-  float* direct = allow_direct && !k_new && pl.single_chunk ? const_cast<float*>(out) : nullptr;
+  // Direct form: for a whole decode whose slabs are single chunks, or a
+  // whole fused step in the two-wave direct form (the kernel then advances
+  // len itself).
+  float* direct = allow_direct && pl.single_chunk && (!k_new || direct_two_waves(pl, d_k, d_v))
+                      ? const_cast<float*>(out)
+                      : nullptr;
+  int32_t* bump = direct && k_new ? const_cast<int32_t*>(len) : nullptr;
   const PartialArgs a{q, const_cast<float*>(K), const_cast<float*>(V), k_new, v_new, len,
-                      scale * kLog2e, B, rows, h_kv, n_max, T, direct};
+                      scale * kLog2e, B, rows, h_kv, n_max, T, direct, bump};
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   if (d_k == 64 && d_v == 64) launch_partial_nb<64, 64>(pl, a, w, s);
@@ -1910,8 +1946,9 @@ da_status da_decode_multi_step(const float* q, float* K, float* V, const float* 
   if (!k_new || !v_new) return DA_ERR_NULL;
   Plan pl;
   da_status st = partial_impl(q, K, V, k_new, v_new, len, scale, B, h_q, h_kv, n_max, d_k, d_v,
-                              T, 0, workspace, workspace_bytes, stream, out, true, &pl);
+                              T, 0, workspace, workspace_bytes, stream, out, true, &pl, true);
   if (st != DA_OK) return st;
+  if (direct_two_waves(pl, d_k, d_v)) return DA_OK;  // the direct form did the whole step
   return merge_impl(out, len, B, h_q, h_kv, n_max, d_k, d_v, T, pl.chunk_rows, workspace,
                     workspace_bytes, stream);
 }

@@ -94,6 +94,8 @@ STEPS = [
     ("mha_d64_T2_full", 2, 4, 4, 64, 64, 300, 2, [299, 300]),   # one row fits / none
     ("mqa_T3_dkdv", 2, 32, 1, 64, 128, 200, 3, [5, 190]),
     ("neg_len_T6", 2, 8, 4, 128, 128, 100, 6, [-3, 40]),
+    # one launch per step (single-segment slabs, G*T <= 16), near capacity
+    ("one_launch_T3", 9, 8, 2, 128, 128, 150, 3, [0, 149, 150, -1, 75, 147, 148, 10, 3]),
 ]
 
 

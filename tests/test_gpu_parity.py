@@ -336,6 +336,10 @@ STEP_CASES = [
     ("mqa32_dkdv", 2, 32, 1, 64, 128, 200, [5, 190]),
     ("neg_len", 2, 8, 4, 128, 128, 100, [-3, 40]),
     ("d256", 2, 8, 2, 256, 256, 400, [0, 399]),
+    # many sequences in the one-launch form (single-segment slabs, G <= 16):
+    # the last workgroup of each sequence advances len
+    ("many_seqs_one_launch", 40, 12, 3, 128, 128, 257,
+     [0, 1, 2, 128, 255, 256, 257, -1, 7, 200] * 4),
 ]
 
 
@@ -360,6 +364,8 @@ def test_fused_step_equals_append_then_decode(cuda_device, case):
         assert dl.cpu().numpy().tolist() == hl.tolist()
         assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))
         assert np.array_equal(dV.cpu().numpy().view(np.uint32), hV.view(np.uint32))
+        nc = binding.workspace_counter_bytes(B, h_q, h_kv, n_max, d_k, d_v)
+        assert not ws[:nc].any(), "counters not back to zero after the step"
         check(out.cpu().numpy().astype(np.float64), ref, f"step {name} t={t}")
 
 
@@ -384,15 +390,17 @@ def test_fused_step_long_context(cuda_device):
         assert dl.cpu().numpy().tolist() == hl.tolist()
 
 
-def test_graph_replay_of_fused_steps(cuda_device):
+@pytest.mark.parametrize("n_max", [1200, 500], ids=["two_launches", "one_launch"])
+def test_graph_replay_of_fused_steps(cuda_device, n_max):
     """Several fused steps captured in one HIP graph and replayed three times,
     each replay from the same initial cache with eager work in between: every
-    replay matches the oracle step by step (the kernel holds no memset and
-    leaves the workspace counters zero, so replays are independent)."""
+    replay matches the oracle step by step (the kernels hold no memset and
+    leave the workspace counters zero, so replays are independent).  At
+    n_max = 500 every slab is one segment and each step is a single launch."""
     T = 4
-    shape = workloads.custom("graph", B=3, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=1200,
+    shape = workloads.custom("graph", B=3, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=n_max,
                              steps=T)
-    inp = workloads.make(shape, seed=21, lens=np.array([0, 600, 1198], np.int32))
+    inp = workloads.make(shape, seed=21, lens=np.array([0, n_max // 2, n_max - 2], np.int32))
     dK0, dV0, dl0 = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
     dK, dV, dl = dK0.clone(), dV0.clone(), dl0.clone()
     qs = [dev(inp.q_step[t], cuda_device) for t in range(T)]
@@ -431,7 +439,7 @@ def test_graph_replay_of_fused_steps(cuda_device):
         assert dl.cpu().numpy().tolist() == hl.tolist()
         assert np.array_equal(dK.cpu().numpy().view(np.uint32), hK.view(np.uint32))
         assert np.array_equal(dV.cpu().numpy().view(np.uint32), hV.view(np.uint32))
-        nc = binding.workspace_counter_bytes(3, 16, 2, 1200, 128, 128)
+        nc = binding.workspace_counter_bytes(3, 16, 2, n_max, 128, 128)
         assert not ws[:nc].any()
 
 
