@@ -110,6 +110,15 @@ constexpr bool kPinQ = NB * DK <= 256;
 constexpr int kChunkQuantum = 12 * kTileRows * kWaves;
 static_assert(12 % 2 == 0 && 12 % 3 == 0 && 12 % 4 == 0, "chunks are whole turns of every ring");
 constexpr int kDefaultChunkRows = 768;
+// Many short slabs: with at least kDirectMinSlabs slabs (four rounds of the
+// 512 two-wave workgroup slots of 256 CUs) of at most kDirectMaxRows rows,
+// one column block and d_k + d_v <= 256, the library takes each slab whole
+// as one segment, so that the direct form runs: one workgroup per slab, two
+// per CU, the hardware dispatcher balancing the slabs and no merge launch.
+// (Measured on uniform and ragged lengths; with fewer slabs, ragged lengths
+// leave the last round's long slabs alone on the chip.)
+constexpr int64_t kDirectMinSlabs = 2048;
+constexpr int kDirectMaxRows = 6 * kChunkQuantum;
 // Visit slots per slab for dynamic visits, in units of the even share of
 // resident workgroups per slab.
 constexpr int kVisitSlack = 4;
@@ -1599,10 +1608,15 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   if (st != DA_OK) return st;
   const int G = h_q / h_kv;
   if (chunk_rows == 0) {
-    // The default, or the whole cache rounded up to the quantum if shorter.
+    // The default, or the whole cache rounded up to the quantum if shorter
+    // or if there are many short slabs (see kDirectMinSlabs).
+    const int64_t whole = ceil_div(n_max, kChunkQuantum) * kChunkQuantum;
+    const int64_t slabs = (int64_t)B * h_kv * ceil_div(G, kHeadsPerGroup);
     chunk_rows = kDefaultChunkRows;
-    chunk_rows = (int)std::min<int64_t>(chunk_rows,
-                                        ceil_div(n_max, kChunkQuantum) * kChunkQuantum);
+    if (G <= kHeadsPerBlock && d_k + d_v <= 256 && slabs >= kDirectMinSlabs &&
+        n_max <= kDirectMaxRows)
+      chunk_rows = (int)whole;
+    chunk_rows = (int)std::min<int64_t>(chunk_rows, whole);
   }
   if (chunk_rows < kChunkQuantum || chunk_rows % kChunkQuantum != 0) return DA_ERR_SHAPE;
   plan->chunk_rows = chunk_rows;

@@ -119,13 +119,30 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     return counters, counters + pad(slots * 8) + slots * d_v * 4
 
 
+def expected_chunk_rows(B, h_q, h_kv, n_max, d_k, d_v):
+    """The library's segment size: 768 rows, or the whole cache rounded up to
+    768 if shorter, or if there are at least 2048 slabs of at most 4608 rows
+    with one column block (G <= 16) and d_k + d_v <= 256 (the direct form)."""
+    whole = -(-n_max // 768) * 768
+    G = h_q // h_kv
+    slabs = B * h_kv * -(-G // 32)
+    c = 768
+    if G <= 16 and d_k + d_v <= 256 and slabs >= 2048 and n_max <= 4608:
+        c = whole
+    return min(c, whole)
+
+
 def test_chunk_rows_and_workspace_sizes():
     for args in [(1, 1, 1, 128, 64, 64), (8, 32, 32, 4112, 128, 128),
                  (16, 32, 8, 8192, 128, 128), (32, 32, 1, 16384, 128, 128),
                  (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128),
-                 (2, 64, 2, 5000, 256, 256), (2, 16, 2, 900, 256, 64)]:
+                 (2, 64, 2, 5000, 256, 256), (2, 16, 2, 900, 256, 64),
+                 (256, 8, 8, 1536, 128, 128), (64, 32, 32, 1040, 128, 128),
+                 (2048, 8, 8, 4608, 64, 64), (2048, 8, 8, 4609, 64, 64),
+                 (1024, 16, 2, 1000, 128, 128), (1024, 17, 1, 1000, 64, 64),
+                 (512, 8, 4, 2000, 128, 256)]:
         c = binding.chunk_rows(*args)
-        assert c == min(768, -(-args[3] // 768) * 768)
+        assert c == expected_chunk_rows(*args), args
         counters, total = _expected_workspace(*args, c)
         assert binding.workspace_counter_bytes(*args) == counters
         assert binding.workspace_bytes(*args) == total
