@@ -1481,28 +1481,39 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
   if (hl >= h_count) return;                            // padding workgroup
   const int tid = threadIdx.x;
   const int64_t row = (int64_t)b * h_q + g * G + hgrp * heads_per_group + hl;
-  const int nv = min((int)nvis[row], J);
   const int ch = tid % kCols;
   const int pv = tid / kCols;
   const float2* ml = ws_ml + row * J;
   const float* acc = ws_acc + row * J * DV;
-
-  // This lane's visits pv, pv + kLanesV, ...: their maximum, then the
-  // rescaled sums (all loads of a pass are independent).
-  float m = -INFINITY;
-#pragma unroll 4
-  for (int jj = pv; jj < nv; jj += kLanesV) m = fmaxf(m, ml[jj].x);
-  float l = 0.f;
-  f4 o = f4{0.f, 0.f, 0.f, 0.f};
-  if (m != -INFINITY) {
-#pragma unroll 4
-    for (int jj = pv; jj < nv; jj += kLanesV) {
-      const float2 st = ml[jj];
-      const float w = fast_exp2(st.x - m);
-      l += st.y * w;
-      o += load4(acc + (int64_t)jj * DV + 4 * ch) * w;
-    }
+  // This lane's first visit (slot pv) is loaded together with the visit
+  // count, before it is known whether the slot holds a visit (it is used
+  // only if it does), so that a head with at most kLanesV visits takes one
+  // round trip to memory.
+  float2 st0 = make_float2(-INFINITY, 0.f);
+  f4 a0 = f4{0.f, 0.f, 0.f, 0.f};
+  if (pv < J) {
+    st0 = ml[pv];
+    a0 = load4(acc + (int64_t)pv * DV + 4 * ch);
   }
+  const int nv = min((int)nvis[row], J);
+
+  // This lane's visits pv, pv + kLanesV, ...: a running reference (the
+  // largest so far), sum and weighted sum, rescaled when the reference
+  // rises; a visit that saw no row (reference -inf) adds nothing.
+  float m = -INFINITY, l = 0.f;
+  f4 o = f4{0.f, 0.f, 0.f, 0.f};
+  auto add = [&](float2 st, f4 a) {
+    if (st.x == -INFINITY) return;
+    const float mn = fmaxf(m, st.x);
+    const float wo = fast_exp2(m - mn);                 // 0 while m = -inf
+    const float wn = fast_exp2(st.x - mn);
+    l = l * wo + st.y * wn;
+    o = o * wo + a * wn;
+    m = mn;
+  };
+  if (pv < nv) add(st0, a0);
+  for (int jj = pv + kLanesV; jj < nv; jj += kLanesV)
+    add(ml[jj], load4(acc + (int64_t)jj * DV + 4 * ch));
   __shared__ float sh_m[kThreads], sh_l[kThreads];
   __shared__ f4 sh_o[kThreads];
   sh_m[tid] = m;
