@@ -6,7 +6,8 @@ head of every sequence gets one new row) followed by decode attention of
 every query head -- run as the fused step, two kernels: the partial kernel
 (which also performs the append) and the merge (which also advances len);
 this is da_decode_step, called as its two halves so that events can bracket
-the partial kernel.  The default workload is
+the partial kernel (a step that da_decode_step runs as one launch, on short
+slabs, is timed whole).  The default workload is
 the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
 len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
 
