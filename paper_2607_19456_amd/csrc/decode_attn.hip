@@ -120,6 +120,11 @@ constexpr int kDefaultChunkRows = 768;
 // (Measured on uniform and ragged lengths; with fewer slabs, ragged lengths
 // leave the last round's long slabs alone on the chip.)
 constexpr int64_t kDirectMinSlabs = 2048;
+// Whole-slab static ranges at two workgroups per CU: from 128 slabs of at
+// most kDirectMaxRows rows.  (Measured: 5-19 % faster than the one-wave
+// schedule on such batches; on longer slabs, whose ranges are long enough
+// for its dynamic balancing and deeper ring to pay, 1.3-7 % slower.)
+constexpr int64_t kTwoWaveMinSlabs = 128;
 constexpr int kDirectMaxRows = 6 * kChunkQuantum;
 // Visit slots per slab for dynamic visits, in units of the even share of
 // resident workgroups per slab.
@@ -920,10 +925,10 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     float* __restrict__ ws_acc, float* __restrict__ out_direct, int32_t* len_bump) {
   // Whole-slab static ranges are planned for one column block only.
   if (NB == 2 && fnum > kStaticNum) fnum = kStaticNum;
-  // Two waves per SIMD serve only the direct form, which schedules nothing
-  // (out_direct is always set there): its scheduling code compiles away.
-  constexpr bool kDirect = W == 2;
-  if constexpr (kDirect) fnum = 0;
+  // Two waves per SIMD serve the direct form (out_direct set; nothing is
+  // scheduled) and whole-slab static ranges (fnum = 16): nothing is claimed
+  // or searched for, so that code compiles away there.
+  constexpr bool kTwo = W == 2;
   const int per_b = h_kv * head_groups;
   const int S = B * per_b;
   const int G = h_q / h_kv;
@@ -967,7 +972,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     }
   };
   // Persistent form: the workgroups share the copies up front.
-  if (!kDirect && app)
+  if (!out_direct && app)
     for (int u = blockIdx.x; u < B * h_kv; u += gridDim.x) append_rows(u, len[u / h_kv]);
   int start = (int)(((int64_t)blockIdx.x * S) / gridDim.x);
   // Direct form (out_direct set; every slab is a single chunk): workgroup s
@@ -997,8 +1002,8 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     // no slab gets more than Jd of them.
     if (wave == 0) {
       int s = -1, j = -1, sr = 0, er = 0, d0 = -1, d1 = -1, dyn = 0;
-      int budget = (kDirect || out_direct || fnum >= kStaticDen) ? 0 : S;
-      if (kDirect || out_direct) {
+      int budget = (kTwo || out_direct || fnum >= kStaticDen) ? 0 : S;
+      if (out_direct) {
         if (first) {
           s = blockIdx.x;
           j = 0;
@@ -1032,7 +1037,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
           ws_s = s;
           ws_st = stb;
           budget = 0;
-          if (u_lo == u_hi && fnum < kStaticDen) {
+          if (!kTwo && u_lo == u_hi && fnum < kStaticDen) {
             // The home visit.  If its static rows do not fill the
             // two-segment window, its first dynamic units are taken now.
             dyn = 1;
@@ -1053,7 +1058,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
           u_lo = u_hi;
         }
       }
-      while (budget > 0) {
+      while (!kTwo && budget > 0) {
         int seen;
         const int cand = find_open_slab(cnt, len, start, budget, S, per_b, n_max, app, T, Cd,
                                         fnum, Jd, lane, &seen);
@@ -1110,7 +1115,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     const int er = sh_ctl[3];
     const int d0 = sh_ctl[4];
     const int d1 = sh_ctl[5];
-    const bool dyn = !kDirect && sh_ctl[6] != 0;
+    const bool dyn = !kTwo && sh_ctl[6] != 0;
     if (s < 0) break;                                   // every slab is exhausted
     first = false;
 
@@ -1432,7 +1437,7 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
   // its first slab) once all its waves are done reading len[b].  The last to
   // check in advances len[b] by the rows that fit and clears the counter for
   // the next call.
-  if (kDirect && app) {
+  if (kTwo && out_direct && app) {
     const int sd = (int)blockIdx.x;
     const int b = sd / per_b;
     const int rem = sd - b * per_b;
@@ -1568,6 +1573,7 @@ struct Plan {
   int Jd;             // dynamic visit slots per slab
   int merge_heads;    // query heads per slab the merge covers
   bool single_chunk;  // every slab fits in one chunk (direct form possible)
+  bool two_waves;     // whole-slab static ranges at two workgroups per CU
   size_t line_bytes, counter_bytes, ml_bytes, bytes;
 };
 
@@ -1649,9 +1655,23 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   if (!plan->single_chunk && B <= kMaxStaticSeqs)
     plan->fnum = plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid
                       ? kStaticDen : kStaticNum;
+  // With at least kTwoWaveMinSlabs slabs of at most kDirectMaxRows rows (one
+  // column block, d_k + d_v <= 256) the rows run as whole-slab ranges at two
+  // workgroups per CU (two waves per SIMD, a two-tile ring): one workgroup's
+  // visit starts and ends overlap the other's streaming, and the ranges,
+  // proportional to the rows, balance ragged batches.  (Independent of the
+  // device's CU count, so that the workspace sized for the largest grid
+  // covers every device.)
+  plan->two_waves = !plan->single_chunk && B <= kMaxStaticSeqs && plan->blocks == 1 &&
+                    d_k + d_v <= 256 && (int64_t)plan->slabs >= kTwoWaveMinSlabs &&
+                    n_max <= kDirectMaxRows;
+  if (plan->two_waves) {
+    plan->grid = (int)std::min<int64_t>(2 * (int64_t)resident, chunks_per_slab * plan->slabs);
+    plan->fnum = kStaticDen;
+  }
   // Scheduling units (static ranges and dynamic hand-outs) are one ring turn
   // of the four waves when there is a static share, else whole chunks.
-  const int ring = ring_tiles(plan->blocks, d_k, d_v);
+  const int ring = plan->two_waves ? 2 : ring_tiles(plan->blocks, d_k, d_v);
   plan->dyn_rows = plan->fnum > 0 ? ring * kWaves * kTileRows : chunk_rows;
   // Static slots: at most one per static unit of a slab plus one, and never
   // more than the workgroups.  Dynamic slots: every dynamic visit holds at
@@ -1717,15 +1737,16 @@ template <int DK, int DV, int NB, bool CAUSAL>
 void launch_partial(const Plan& pl, const PartialArgs& a, const WsView& w, hipStream_t stream) {
   // The direct form runs one workgroup per slab; otherwise the resident grid.
   const unsigned grid = a.out_direct ? (unsigned)pl.slabs : (unsigned)pl.grid;
-  // The direct form schedules nothing: no static share.  (The two-wave
-  // instances are the shapes direct_two_waves() names.)
+  // The direct form schedules nothing: no static share.  The two-wave
+  // instances run the direct form of the shapes direct_two_waves() names
+  // and the two-wave whole-slab ranges.
   if constexpr (NB == 1 && DK + DV <= 256) {
-    if (a.out_direct) {
+    if (a.out_direct || pl.two_waves) {
       hipLaunchKernelGGL((decode_partial_kernel<DK, DV, NB, CAUSAL, 2>), dim3(grid),
                          dim3(kThreads), 0, stream, a.q, a.K, a.V, a.k_new, a.v_new, a.len,
                          a.qscale, a.B, a.h_q, a.h_kv, a.n_max, a.T, pl.chunk_rows, pl.dyn_rows,
-                         0, pl.head_groups, pl.J, pl.Jd, w.cnt, w.nvis, w.ml, w.acc,
-                         a.out_direct, a.len_bump);
+                         a.out_direct ? 0 : pl.fnum, pl.head_groups, pl.J, pl.Jd, w.cnt, w.nvis,
+                         w.ml, w.acc, a.out_direct, a.len_bump);
       return;
     }
   }

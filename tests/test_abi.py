@@ -100,7 +100,9 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     resident workgroups per slab (at most one per unit); one 128-byte
     counter line per slab and one visit count per (b, query head).
     Single-chunk caches and batches of more than 256 sequences are scheduled
-    dynamically only, in whole chunks."""
+    dynamically only, in whole chunks.  From 128 slabs of at most 4608 rows
+    on (one column block, d_k + d_v <= 256) whole-slab ranges run at two
+    workgroups per CU with a two-tile ring."""
     pad = lambda x: -(-x // 256) * 256
     G = h_q // h_kv
     groups = -(-G // 32)
@@ -110,6 +112,9 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     grid = max(1, min(resident, chunks * slabs))
     static = chunks > 1 and B <= 256
     ring = 2 if d_k + d_v > 256 else (4 if G > 16 else 3)
+    if static and G <= 16 and d_k + d_v <= 256 and slabs >= 128 and n_max <= 4608:
+        grid = min(2 * resident, chunks * slabs)
+        ring = 2
     dyn_rows = ring * 64 if static else c
     Js = min(grid, -(-n_max // dyn_rows)) + 1 if static else 0
     Jd = max(1, min(-(-n_max // dyn_rows), 4 * -(-grid // slabs)))
@@ -140,7 +145,8 @@ def test_chunk_rows_and_workspace_sizes():
                  (256, 8, 8, 1536, 128, 128), (64, 32, 32, 1040, 128, 128),
                  (2048, 8, 8, 4608, 64, 64), (2048, 8, 8, 4609, 64, 64),
                  (1024, 16, 2, 1000, 128, 128), (1024, 17, 1, 1000, 64, 64),
-                 (512, 8, 4, 2000, 128, 256)]:
+                 (512, 8, 4, 2000, 128, 256), (128, 32, 8, 8192, 128, 128),
+                 (256, 16, 4, 2048, 64, 64), (1024, 8, 1, 5000, 128, 128)]:
         c = binding.chunk_rows(*args)
         assert c == expected_chunk_rows(*args), args
         counters, total = _expected_workspace(*args, c)

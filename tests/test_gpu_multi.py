@@ -96,6 +96,8 @@ STEPS = [
     ("neg_len_T6", 2, 8, 4, 128, 128, 100, 6, [-3, 40]),
     # one launch per step (single-segment slabs, G*T <= 16), near capacity
     ("one_launch_T3", 9, 8, 2, 128, 128, 150, 3, [0, 149, 150, -1, 75, 147, 148, 10, 3]),
+    # 1024 slabs: whole-slab ranges at two workgroups per CU, causal rows
+    ("two_wave_T2", 128, 8, 8, 64, 64, 900, 2, [0, 1, 898, 899, 900, 450, 3, 777] * 16),
 ]
 
 

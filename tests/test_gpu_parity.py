@@ -293,6 +293,10 @@ SCHEDULE = [
     # two column blocks: the full resident grid of two workgroups per CU
     # (interleaved ranks) on a ragged batch
     ("two_blocks_ragged", 8, 64, 2, 64, 64, 16384, "ragged"),
+    # 1024 slabs or more of multi-segment caches: whole-slab ranges at two
+    # workgroups per CU (512 ranges), a range walking several slabs
+    ("two_wave_ranges", 128, 16, 8, 64, 64, 1000, "ragged"),
+    ("two_wave_wide_sequences", 8, 128, 128, 128, 128, 900, "ragged"),
 ]
 
 
@@ -340,6 +344,10 @@ STEP_CASES = [
     # the last workgroup of each sequence advances len
     ("many_seqs_one_launch", 40, 12, 3, 128, 128, 257,
      [0, 1, 2, 128, 255, 256, 257, -1, 7, 200] * 4),
+    # 1024 slabs of multi-segment caches: whole-slab ranges at two
+    # workgroups per CU, then the merge
+    ("two_wave_ranges_step", 128, 8, 8, 128, 128, 1200,
+     [0, 1, 799, 800, 1199, 1200, -2, 500] * 16),
 ]
 
 
