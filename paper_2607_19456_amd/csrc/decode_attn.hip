@@ -120,11 +120,6 @@ constexpr int kDefaultChunkRows = 768;
 // (Measured on uniform and ragged lengths; with fewer slabs, ragged lengths
 // leave the last round's long slabs alone on the chip.)
 constexpr int64_t kDirectMinSlabs = 2048;
-// Whole-slab static ranges at two workgroups per CU: from 128 slabs of at
-// most kDirectMaxRows rows.  (Measured: 5-19 % faster than the one-wave
-// schedule on such batches; on longer slabs, whose ranges are long enough
-// for its dynamic balancing and deeper ring to pay, 1.3-7 % slower.)
-constexpr int64_t kTwoWaveMinSlabs = 128;
 constexpr int kDirectMaxRows = 6 * kChunkQuantum;
 // Visit slots per slab for dynamic visits, in units of the even share of
 // resident workgroups per slab.
@@ -1655,16 +1650,18 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   if (!plan->single_chunk && B <= kMaxStaticSeqs)
     plan->fnum = plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid
                       ? kStaticDen : kStaticNum;
-  // With at least kTwoWaveMinSlabs slabs of at most kDirectMaxRows rows (one
-  // column block, d_k + d_v <= 256) the rows run as whole-slab ranges at two
-  // workgroups per CU (two waves per SIMD, a two-tile ring): one workgroup's
-  // visit starts and ends overlap the other's streaming, and the ranges,
-  // proportional to the rows, balance ragged batches.  (Independent of the
-  // device's CU count, so that the workspace sized for the largest grid
-  // covers every device.)
+  // Slabs of at most kDirectMaxRows rows (one column block, d_k + d_v <=
+  // 256) run as whole-slab ranges at two workgroups per CU (two waves per
+  // SIMD, a two-tile ring): one workgroup's visit starts and ends overlap
+  // the other's streaming, and the ranges, proportional to the rows, balance
+  // ragged batches.  Measured 2-22 % faster than the one-wave schedule on
+  // such caches (the most on small, latency-bound batches); on longer slabs,
+  // whose ranges are long enough for the one-wave schedule's deeper ring and
+  // dynamic balancing to pay, 1.3-7 % slower.  (Independent of the device's
+  // CU count, so that the workspace sized for the largest grid covers every
+  // device.)
   plan->two_waves = !plan->single_chunk && B <= kMaxStaticSeqs && plan->blocks == 1 &&
-                    d_k + d_v <= 256 && (int64_t)plan->slabs >= kTwoWaveMinSlabs &&
-                    n_max <= kDirectMaxRows;
+                    d_k + d_v <= 256 && n_max <= kDirectMaxRows;
   if (plan->two_waves) {
     plan->grid = (int)std::min<int64_t>(2 * (int64_t)resident, chunks_per_slab * plan->slabs);
     plan->fnum = kStaticDen;

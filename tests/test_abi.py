@@ -100,8 +100,8 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     resident workgroups per slab (at most one per unit); one 128-byte
     counter line per slab and one visit count per (b, query head).
     Single-chunk caches and batches of more than 256 sequences are scheduled
-    dynamically only, in whole chunks.  From 128 slabs of at most 4608 rows
-    on (one column block, d_k + d_v <= 256) whole-slab ranges run at two
+    dynamically only, in whole chunks.  Caches of at most 4608 rows (one
+    column block, d_k + d_v <= 256) run as whole-slab ranges at two
     workgroups per CU with a two-tile ring."""
     pad = lambda x: -(-x // 256) * 256
     G = h_q // h_kv
@@ -112,7 +112,7 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     grid = max(1, min(resident, chunks * slabs))
     static = chunks > 1 and B <= 256
     ring = 2 if d_k + d_v > 256 else (4 if G > 16 else 3)
-    if static and G <= 16 and d_k + d_v <= 256 and slabs >= 128 and n_max <= 4608:
+    if static and G <= 16 and d_k + d_v <= 256 and n_max <= 4608:
         grid = min(2 * resident, chunks * slabs)
         ring = 2
     dyn_rows = ring * 64 if static else c
