@@ -6,8 +6,10 @@ head of every sequence gets one new row) followed by decode attention of
 every query head -- run as the fused step, two kernels: the partial kernel
 (which also performs the append) and the merge (which also advances len);
 this is da_decode_step, called as its two halves so that events can bracket
-the partial kernel (a step that da_decode_step runs as one launch, on short
-slabs, is timed whole).  The default workload is
+the partial kernel in a second pass over the same steps (a step that
+da_decode_step runs as one launch, on short slabs, is timed whole there).
+The timed region itself holds only the K steps' launches: an event recorded
+between two launches delays the second.  The default workload is
 the long-context ragged GQA configuration (B=4, h_q=64, h_kv=8, d=128,
 len ~ U{65536..131008}, n_max=131072, 64 append+decode steps).
 
@@ -19,7 +21,8 @@ Prints ONE JSON line:
                HBM before the timed region starts.
   roofline     the dominant kernel (decode_partial_kernel): its algorithmic
                bytes per launch over its average launch duration, measured with
-               HIP events on the stream it runs on, against the 8 TB/s HBM peak;
+               HIP events on the stream it runs on (in the second pass over the
+               same K steps), against the 8 TB/s HBM peak;
                `traffic` = HBM bytes per launch from rocprofv3 FETCH_SIZE and
                WRITE_SIZE counters (profiles/decode_partial_counters.json),
                null when the kernel source changed since they were taken;
@@ -436,11 +439,10 @@ def main() -> int:
 
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
-    merge_ms = None
     if args.graph:
         # The timed steps as one graph (the graph holds no memset, and the
         # workspace counters come back to zero after each step), replayed once
-        # from the same initial state; the per-launch time is then the step's.
+        # from the same initial state.
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             for i in range(args.steps):
@@ -461,26 +463,39 @@ def main() -> int:
         graph.replay()
         end.record(stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - wall0
-        total_ms = start.elapsed_time(end)
-        launch_ms = [total_ms / args.steps] * args.steps
     else:
-        ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-        ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-        ev_c = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        # The K steps back to back, with nothing but their own launches on
+        # the stream between the two events.
         log(f"timing {args.steps} step(s)")
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
         start.record(stream)
         for i in range(args.steps):
-            step(i, ev_a[i], ev_b[i], ev_c[i])
+            step(i)
         end.record(stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - wall0
-        total_ms = start.elapsed_time(end)
-        launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
-        if not (multi or direct or direct_step):
-            merge_ms = [b.elapsed_time(c) for b, c in zip(ev_b, ev_c)]
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+
+    # Per-launch durations for the roofline: the same K steps once more, from
+    # the same initial state, each launch bracketed by events.  They stay out
+    # of the timed region above because every event recorded between two
+    # launches holds the next one back (about 3 us each; three per step made
+    # a long-context step ~10 us longer).
+    dl.copy_(lens0)
+    torch.cuda.synchronize()
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_c = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(i, ev_a[i], ev_b[i], ev_c[i])
+    torch.cuda.synchronize()
+    launch_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
+    merge_ms = None
+    if not (multi or direct or direct_step):
+        merge_ms = [b.elapsed_time(c) for b, c in zip(ev_b, ev_c)]
+    log(f"per-launch pass: {sum(launch_ms) / len(launch_ms) * 1e3:.1f} us per "
+        + ("step" if (multi or direct or direct_step) else "partial launch"))
 
     def step_bytes(lens, with_append=True):
         b = traffic.batch_decode_bytes(lens, s.h_q, s.h_kv, s.d_k, s.d_v, s.rows)
@@ -533,6 +548,8 @@ def main() -> int:
         },
         "settle_steps_untimed": settled,
         "us_per_step": round(ms_per_step * 1e3, 2),
+        "step_timing": ("one graph replay of the K steps between two events" if args.graph
+                        else "two events around the K steps, none between them"),
         "hbm_roofline_frac_step": round(value / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": int(alg_bytes / args.steps),
         "host_wall_s": round(wall, 4),
@@ -549,9 +566,10 @@ def main() -> int:
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": None if multi else counter_traffic(s.name),
             "avg_launch_us": round(launch_avg_ms * 1e3, 2),
-            "timing": ("graph replay / steps" if args.graph
-                       else "HIP events around each step" if multi or direct or direct_step
-                       else "HIP events around each partial launch"),
+            "timing": ("HIP events around each step" if multi or direct or direct_step
+                       else "HIP events around each partial launch")
+                      + ", in a second pass over the same K steps (the timed region has "
+                        "no events between its launches)",
             "algorithmic_bytes_per_launch": int(sum(launch_bytes) / len(launch_bytes)),
         },
     }
