@@ -79,8 +79,9 @@ constexpr int kMaxResident = 256;
 // Register tiles per wave in the load ring of the partial kernel, which
 // runs one wave per SIMD (all 512 registers of a lane).  One column block
 // (<= 16 query rows per KV head): a three-tile ring keeps two tiles' loads in
-// flight during each tile's products (two tiles at two waves per SIMD
-// measured the same on long contexts and 2-3 % slower on the shorter ones).
+// flight during each tile's products (two-tile rings at two waves per SIMD
+// measured 2-4 % slower with fixed splits, and with the dynamic units below
+// 10-30 % slower on long slabs).
 // Two column blocks double the matrix work per tile: a four-tile ring (three
 // tiles in flight), with both blocks' score chains, softmax updates and
 // weighted sums issued side by side, is 6 % faster on MQA than a two-tile
