@@ -308,6 +308,14 @@ da_status da_decode_attn_noalloc(const float *q, const float *K,
  * A workspace sized by da_decode_workspace_bytes_ex for some chunk_rows
  * serves only calls with that chunk_rows.  DA_ERR_SHAPE also covers an
  * invalid chunk_rows.
+ *
+ * The environment variable DECODE_ATTN_DYNAMIC_MIN_UNITS (a non-negative
+ * integer, read at every call; default 32) is the fewest scheduling units
+ * per resident workgroup, counted at n_max rows per slab, for which a decode
+ * keeps part of each slab for dynamic hand-out; below it every slab is
+ * divided in advance.  0 keeps the dynamic part wherever the schedule has
+ * one (tests use it to cover that path on small caches).  It changes neither
+ * the workspace size nor the results beyond fp32 rounding.
  * ---------------------------------------------------------------------------
  */
 

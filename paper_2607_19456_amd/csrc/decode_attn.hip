@@ -49,6 +49,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdint>
+#include <cstdlib>
 
 #include "decode_attn.h"
 
@@ -136,6 +137,16 @@ constexpr int kVisitSlack = 4;
 constexpr int kStaticDen = 16;
 constexpr int kStaticNum = 14;
 constexpr int kMaxStaticSeqs = 256;
+// The dynamic share pays only where each workgroup holds enough units for it
+// to move: a workgroup commits two to three units ahead, so with fewer than
+// kDynamicMinUnits units per resident workgroup (counted at n_max rows per
+// slab) every slab is wholly static instead -- no claims, no per-unit
+// barriers, no dynamic visits.  (Measured: MQA 16384 rows 2.7 % faster, short
+// and ragged batches of 10-22 units per workgroup 5-10 % faster, batches of
+// 43 units per workgroup level to 2 % slower, longer ones unchanged.)  The
+// environment variable DECODE_ATTN_DYNAMIC_MIN_UNITS overrides the bound (0:
+// the static share wherever it applied before; for tests and tuning).
+constexpr int kDynamicMinUnits = 32;
 constexpr int64_t kMaxSlabs = 1 << 20;
 constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
 // Each slab's scheduling word, {dynamic units taken (low half), dynamic
@@ -919,8 +930,6 @@ __global__ __launch_bounds__(kThreads, W) void decode_partial_kernel(
     int B, int h_q, int h_kv, int n_max, int T, int C, int Cd, int fnum, int head_groups, int J,
     int Jd, unsigned* __restrict__ cnt, unsigned* __restrict__ nvis, float2* __restrict__ ws_ml,
     float* __restrict__ ws_acc, float* __restrict__ out_direct, int32_t* len_bump) {
-  // Whole-slab static ranges are planned for one column block only.
-  if (NB == 2 && fnum > kStaticNum) fnum = kStaticNum;
   // Two waves per SIMD serve the direct form (out_direct set; nothing is
   // scheduled) and whole-slab static ranges (fnum = 16): nothing is claimed
   // or searched for, so that code compiles away there.
@@ -1613,6 +1622,15 @@ int device_resident() {
   return c;
 }
 
+// kDynamicMinUnits, or the environment's override (read at every call).
+int dynamic_min_units() {
+  const char* e = std::getenv("DECODE_ATTN_DYNAMIC_MIN_UNITS");
+  if (!e || !*e) return kDynamicMinUnits;
+  char* end = nullptr;
+  const long v = std::strtol(e, &end, 10);
+  return (*end == 0 && v >= 0 && v <= (1L << 20)) ? (int)v : kDynamicMinUnits;
+}
+
 // The work decomposition for these shapes with `resident` resident
 // workgroups.  Every size below grows with `resident`, so the plan for
 // kMaxResident bounds the workspace of any device's plan.
@@ -1644,13 +1662,19 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   plan->grid = (int)std::max<int64_t>(1, std::min<int64_t>(resident, chunks_per_slab * plan->slabs));
   // Static share: off for single-chunk caches (direct form) and for batches
   // whose per-workgroup prefix over sequences would be long.  With two or
-  // more slabs per workgroup the even split of whole slabs balances the
-  // grid by itself and the dynamic searches over many slabs are saved
-  // (one column block only: with two, whole slabs measured 0-1.5 % slower).
+  // more slabs per workgroup (one column block) the even split of whole
+  // slabs balances the grid by itself and the dynamic searches over many
+  // slabs are saved (with two column blocks and many slabs the dynamic
+  // remainders measured 0-1.5 % faster); with few units per workgroup the
+  // dynamic share cannot move work (kDynamicMinUnits).
   plan->fnum = 0;
-  if (!plan->single_chunk && B <= kMaxStaticSeqs)
-    plan->fnum = plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid
-                      ? kStaticDen : kStaticNum;
+  if (!plan->single_chunk && B <= kMaxStaticSeqs) {
+    const int64_t units =
+        (int64_t)plan->slabs * ceil_div(n_max, ring_tiles(plan->blocks, d_k, d_v) * kWaves * kTileRows);
+    const bool few = units < (int64_t)dynamic_min_units() * plan->grid;
+    plan->fnum = (plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid) || few
+                     ? kStaticDen : kStaticNum;
+  }
   // Slabs of at most kDirectMaxRows rows (one column block, d_k + d_v <=
   // 256) run as whole-slab ranges at two workgroups per CU (two waves per
   // SIMD, a two-tile ring): one workgroup's visit starts and ends overlap

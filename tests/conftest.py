@@ -26,3 +26,16 @@ def cuda_device():
     import torch
     assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
     return torch.device("cuda:0")
+
+
+@pytest.fixture(params=["default", "dynamic"])
+def schedule(request, monkeypatch):
+    """Run a test under the library's own schedule and with the dynamic share
+    wherever the planner allows one (DECODE_ATTN_DYNAMIC_MIN_UNITS=0): small
+    caches are otherwise wholly static, and the dynamic units, visits and
+    claims must stay covered by small, oracle-checked shapes too."""
+    if request.param == "dynamic":
+        monkeypatch.setenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", "0")
+    else:
+        monkeypatch.delenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", raising=False)
+    return request.param

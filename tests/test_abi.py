@@ -162,6 +162,19 @@ def test_chunk_rows_and_workspace_sizes():
     assert lib.da_decode_workspace_bytes(1, 3, 2, 10, 64, 64) == 0
 
 
+@pytest.mark.parametrize("value", ["0", "32", "1000", "bad", ""])
+def test_dynamic_share_override_leaves_sizes_alone(monkeypatch, value):
+    """The tuning override of the dynamic share (DECODE_ATTN_DYNAMIC_MIN_UNITS,
+    read at every call) changes which rows are scheduled how, never the
+    workspace a caller must provide or the segment size."""
+    args = [(32, 32, 1, 16384, 128, 128), (16, 32, 8, 8192, 128, 128),
+            (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]
+    monkeypatch.delenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", raising=False)
+    ref = [(lib.da_decode_workspace_bytes(*a), binding.chunk_rows(*a)) for a in args]
+    monkeypatch.setenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", value)
+    assert [(lib.da_decode_workspace_bytes(*a), binding.chunk_rows(*a)) for a in args] == ref
+
+
 def _decode(**kw):
     """da_decode_attn, or with ``chunk`` its tuning form da_decode_multi_ex."""
     a = dict(q=FAKE, K=FAKE, V=FAKE, len=FAKE, scale=0.125, out=FAKE, B=1, h_q=1,

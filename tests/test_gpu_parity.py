@@ -197,7 +197,7 @@ def test_plain_decode_leaves_cache_and_len_alone(cuda_device):
 
 
 @pytest.mark.parametrize("h_q,h_kv", [(4, 1), (1, 1), (32, 1)])
-def test_one_slab_many_visits(cuda_device, h_q, h_kv):
+def test_one_slab_many_visits(cuda_device, schedule, h_q, h_kv):
     """A single long slab in small chunks: every resident workgroup visits it,
     so its merge combines hundreds of partials."""
     n = 150_000
@@ -287,8 +287,9 @@ SCHEDULE = [
     # more sequences than the static part handles: dynamic units of whole
     # segments only, on multi-segment slabs
     ("many_sequences_dynamic", 300, 4, 2, 64, 64, 1000, "ragged"),
-    # two column blocks with many slabs per workgroup keep the 14/16 static
-    # share with dynamic remainders
+    # two column blocks with many slabs per workgroup: the 14/16 static share
+    # with dynamic remainders where they pay (here only under the fixture's
+    # dynamic schedule: 16 units per workgroup)
     ("two_blocks_many_slabs", 128, 256, 8, 64, 64, 800, "ragged"),
     # two column blocks: the full resident grid of two workgroups per CU
     # (interleaved ranks) on a ragged batch
@@ -301,7 +302,7 @@ SCHEDULE = [
 
 
 @pytest.mark.parametrize("case", SCHEDULE, ids=[c[0] for c in SCHEDULE])
-def test_schedule_edge_cases(cuda_device, case):
+def test_schedule_edge_cases(cuda_device, schedule, case):
     """Static ranges and dynamic units cover every row exactly once however
     the lengths fall: compared with the oracle, with NaN-poisoned partial
     slots (a slot never written would show)."""

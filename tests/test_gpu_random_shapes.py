@@ -2,8 +2,10 @@
 
 Every combination the planner distinguishes -- one or two MFMA column
 blocks, several head groups, d_k != d_v, head sizes 64/128/256, the direct
-form (single-chunk caches), the 14/16 static share with dynamic units,
-whole-slab ranges (many slabs), large batches scheduled dynamically only,
+form (single-chunk caches), the 14/16 static share with dynamic units
+(forced where the planner would make a small cache wholly static: the
+``schedule`` fixture runs every case both ways), whole-slab ranges (many
+slabs), large batches scheduled dynamically only,
 empty and full caches -- is drawn from one fixed seed, so a failure names a
 reproducible case.  Decode: max-abs-err <= 1e-5 with the cache rows beyond
 len[b] poisoned with NaN; the fused step (append + decode) also checks the
@@ -93,7 +95,7 @@ def _inputs(case, steps=0):
 
 
 @pytest.mark.parametrize("case", DECODE_CASES, ids=[c[0] for c in DECODE_CASES])
-def test_random_shape_decode(cuda_device, case):
+def test_random_shape_decode(cuda_device, schedule, case):
     shape, inp, chunk = _inputs(case)
     say(f"decode {case[0]} lens={inp.lens.tolist()[:8]}")
     dq, dK, dV = dev(inp.q, cuda_device), dev(inp.K, cuda_device), dev(inp.V, cuda_device)
@@ -109,7 +111,7 @@ def test_random_shape_decode(cuda_device, case):
 
 
 @pytest.mark.parametrize("case", STEP_CASES, ids=[c[0] for c in STEP_CASES])
-def test_random_shape_fused_step(cuda_device, case):
+def test_random_shape_fused_step(cuda_device, schedule, case):
     shape, inp, chunk = _inputs(case, steps=2)
     dK, dV, dl = dev(inp.K, cuda_device), dev(inp.V, cuda_device), dev(inp.lens, cuda_device)
     hK, hV, hl = inp.K.copy(), inp.V.copy(), inp.lens.copy()
