@@ -21,7 +21,9 @@
 // Work decomposition of decode_partial_kernel
 //   A resident grid of 256-thread workgroups (4 waves) shares the slabs' rows:
 //   most of each slab in ranges fixed in advance, proportional to the
-//   lengths, the rest in small units handed out by per-slab counters; a
+//   lengths, the rest in small units handed out by per-slab counters (all
+//   of it in ranges where a workgroup would hold too few units for the
+//   hand-out to move work); a
 //   workgroup's four waves share each 64-row turn of a segment, 16 rows
 //   each (with one column block the waves' rows interleave in groups of
 //   256/d rows, so the four waves' loads of one instruction cover 4 KB of
