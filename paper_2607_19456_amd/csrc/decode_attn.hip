@@ -149,6 +149,15 @@ constexpr int kMaxStaticSeqs = 256;
 // environment variable DECODE_ATTN_DYNAMIC_MIN_UNITS overrides the bound (0:
 // the static share wherever it applied before; for tests and tuning).
 constexpr int kDynamicMinUnits = 32;
+// A batch of fewer than kTwoWaveMaxUnits one-wave units per CU of the
+// largest grid (counted at n_max rows per slab) runs, with one column block
+// and a wholly static plan, as whole-slab ranges at two workgroups per CU
+// whatever its slabs' length: one workgroup's visit set-up and drain overlap
+// the other's streaming.  Measured on batches of 1-4 sequences of 16-64k
+// rows (8-16 units per workgroup): 5.7-8.4 % faster; at 22 units per
+// workgroup (MHA 8 x 32 heads x 4112 rows, GQA-4 16 x 8192 rows) 0.1-0.4 %
+// slower, so those keep one workgroup per CU.
+constexpr int kTwoWaveMaxUnits = 16;
 constexpr int64_t kMaxSlabs = 1 << 20;
 constexpr int kMaxQueryRows = 4096;                  // T of a multi-row decode
 // Each slab's scheduling word, {dynamic units taken (low half), dynamic
@@ -1669,14 +1678,13 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   // slabs are saved (with two column blocks and many slabs the dynamic
   // remainders measured 0-1.5 % faster); with few units per workgroup the
   // dynamic share cannot move work (kDynamicMinUnits).
+  const int64_t units =
+      (int64_t)plan->slabs * ceil_div(n_max, ring_tiles(plan->blocks, d_k, d_v) * kWaves * kTileRows);
+  const bool few = units < (int64_t)dynamic_min_units() * plan->grid;
   plan->fnum = 0;
-  if (!plan->single_chunk && B <= kMaxStaticSeqs) {
-    const int64_t units =
-        (int64_t)plan->slabs * ceil_div(n_max, ring_tiles(plan->blocks, d_k, d_v) * kWaves * kTileRows);
-    const bool few = units < (int64_t)dynamic_min_units() * plan->grid;
+  if (!plan->single_chunk && B <= kMaxStaticSeqs)
     plan->fnum = (plan->blocks == 1 && (int64_t)plan->slabs >= 2 * (int64_t)plan->grid) || few
                      ? kStaticDen : kStaticNum;
-  }
   // Slabs of at most kDirectMaxRows rows (one column block, d_k + d_v <=
   // 256) run as whole-slab ranges at two workgroups per CU (two waves per
   // SIMD, a two-tile ring): one workgroup's visit starts and ends overlap
@@ -1686,9 +1694,12 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   // whose ranges are long enough for the one-wave schedule's deeper ring and
   // dynamic balancing to pay, 1.3-7 % slower.  (Independent of the device's
   // CU count, so that the workspace sized for the largest grid covers every
-  // device.)
-  plan->two_waves = !plan->single_chunk && B <= kMaxStaticSeqs && plan->blocks == 1 &&
-                    d_k + d_v <= 256 && n_max <= kDirectMaxRows;
+  // device.)  Longer slabs take the same form when the whole batch is short
+  // (kTwoWaveMaxUnits) and the static plan applies.
+  const bool tw_base = !plan->single_chunk && B <= kMaxStaticSeqs && plan->blocks == 1 &&
+                       d_k + d_v <= 256;
+  const bool tw_short_batch = units < (int64_t)kTwoWaveMaxUnits * kMaxResident;
+  plan->two_waves = tw_base && (n_max <= kDirectMaxRows || (tw_short_batch && few));
   if (plan->two_waves) {
     plan->grid = (int)std::min<int64_t>(2 * (int64_t)resident, chunks_per_slab * plan->slabs);
     plan->fnum = kStaticDen;
@@ -1706,7 +1717,19 @@ da_status make_plan(int B, int h_q, int h_kv, int n_max, int d_k, int d_v, int c
   const int64_t share = ceil_div((int64_t)plan->grid, plan->slabs);
   plan->Jd = (int)std::max<int64_t>(
       1, std::min(ceil_div(n_max, plan->dyn_rows), kVisitSlack * share));
-  plan->J = (int)(Js + plan->Jd);
+  int64_t J = Js + plan->Jd;
+  if (tw_base && tw_short_batch && !plan->two_waves) {
+    // The slots of the two-wave form, which the same shapes take under
+    // another DECODE_ATTN_DYNAMIC_MIN_UNITS: the workspace a caller sizes
+    // must not depend on the environment.
+    const int64_t g2 = std::min<int64_t>(2 * (int64_t)resident, chunks_per_slab * plan->slabs);
+    const int64_t r2 = 2 * kWaves * kTileRows;
+    const int64_t J2 = std::min<int64_t>(g2, ceil_div(n_max, r2)) + 1 +
+                       std::max<int64_t>(1, std::min(ceil_div(n_max, r2),
+                                                     kVisitSlack * ceil_div(g2, plan->slabs)));
+    J = std::max(J, J2);
+  }
+  plan->J = (int)J;
   const size_t heads = (size_t)B * h_q;
   const size_t slots = heads * plan->J;
   plan->line_bytes = pad256((size_t)plan->slabs * kCounterStride * sizeof(unsigned));

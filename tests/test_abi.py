@@ -102,7 +102,9 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     Single-chunk caches and batches of more than 256 sequences are scheduled
     dynamically only, in whole chunks.  Caches of at most 4608 rows (one
     column block, d_k + d_v <= 256) run as whole-slab ranges at two
-    workgroups per CU with a two-tile ring."""
+    workgroups per CU with a two-tile ring, and so may batches of fewer
+    than 16 * 256 one-wave units (192 rows each) of any length: the
+    workspace is sized for that form whenever it may be chosen."""
     pad = lambda x: -(-x // 256) * 256
     G = h_q // h_kv
     groups = -(-G // 32)
@@ -112,7 +114,8 @@ def _expected_workspace(B, h_q, h_kv, n_max, d_k, d_v, c):
     grid = max(1, min(resident, chunks * slabs))
     static = chunks > 1 and B <= 256
     ring = 2 if d_k + d_v > 256 else (4 if G > 16 else 3)
-    if static and G <= 16 and d_k + d_v <= 256 and n_max <= 4608:
+    units = slabs * -(-n_max // (ring * 64))
+    if static and G <= 16 and d_k + d_v <= 256 and (n_max <= 4608 or units < 16 * resident):
         grid = min(2 * resident, chunks * slabs)
         ring = 2
     dyn_rows = ring * 64 if static else c
@@ -146,7 +149,9 @@ def test_chunk_rows_and_workspace_sizes():
                  (2048, 8, 8, 4608, 64, 64), (2048, 8, 8, 4609, 64, 64),
                  (1024, 16, 2, 1000, 128, 128), (1024, 17, 1, 1000, 64, 64),
                  (512, 8, 4, 2000, 128, 256), (128, 32, 8, 8192, 128, 128),
-                 (256, 16, 4, 2048, 64, 64), (1024, 8, 1, 5000, 128, 128)]:
+                 (256, 16, 4, 2048, 64, 64), (1024, 8, 1, 5000, 128, 128),
+                 (2, 32, 8, 32768, 128, 128), (1, 32, 8, 65536, 128, 128),
+                 (4, 32, 8, 16384, 64, 64), (16, 16, 4, 16384, 128, 128)]:
         c = binding.chunk_rows(*args)
         assert c == expected_chunk_rows(*args), args
         counters, total = _expected_workspace(*args, c)
@@ -168,7 +173,8 @@ def test_dynamic_share_override_leaves_sizes_alone(monkeypatch, value):
     read at every call) changes which rows are scheduled how, never the
     workspace a caller must provide or the segment size."""
     args = [(32, 32, 1, 16384, 128, 128), (16, 32, 8, 8192, 128, 128),
-            (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128)]
+            (4, 64, 8, 131072, 128, 128), (3, 40, 5, 77, 64, 128),
+            (2, 32, 8, 32768, 128, 128), (1, 32, 8, 65536, 128, 128)]
     monkeypatch.delenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", raising=False)
     ref = [(lib.da_decode_workspace_bytes(*a), binding.chunk_rows(*a)) for a in args]
     monkeypatch.setenv("DECODE_ATTN_DYNAMIC_MIN_UNITS", value)
