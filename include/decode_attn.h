@@ -136,12 +136,15 @@ da_status da_decode_workspace_reset(void *workspace, size_t workspace_bytes,
  * launch combines the partials exactly (a regrouping of eqs. (2)-(3) over
  * disjoint row sets).  Which workgroup takes which dynamic unit varies, so
  * the summation order varies from call to call within fp32 rounding.  Short
- * caches (n_max <= 4608, h_q / h_kv <= 16, d_k + d_v <= 256) are cut into
- * row ranges only, run at two workgroups per CU.  When every slab is a
- * single segment (n_max <= 768, or at least 2048 (b, KV head) slabs with
- * n_max <= 4608, h_q / h_kv <= 16 and d_k + d_v <= 256) the decode is a
- * single launch that writes out directly.  Equivalent to da_decode_partial
- * followed by da_decode_merge.
+ * caches (n_max <= 4608, h_q / h_kv <= 16, d_k + d_v <= 256), and short
+ * batches of such heads whatever their length (fewer than 16 * 256 units of
+ * 192 rows over all slabs), are cut into row ranges only, run at two
+ * workgroups per CU; so are other batches too short for the dynamic units
+ * to move work (fewer than 32 units per workgroup), at one per CU.  When
+ * every slab is a single segment (n_max <= 768, or at least 2048 (b, KV
+ * head) slabs with n_max <= 4608, h_q / h_kv <= 16 and d_k + d_v <= 256) the
+ * decode is a single launch that writes out directly.  Equivalent to
+ * da_decode_partial followed by da_decode_merge.
  *
  * Supported: d_k, d_v in {64, 128, 256}; any B, h_q, h_kv >= 1 with h_kv | h_q.
  * workspace: see above; at least da_decode_workspace_bytes(...) bytes,
