@@ -399,13 +399,16 @@ def test_fused_step_long_context(cuda_device):
         assert dl.cpu().numpy().tolist() == hl.tolist()
 
 
-@pytest.mark.parametrize("n_max", [1200, 500], ids=["two_launches", "one_launch"])
-def test_graph_replay_of_fused_steps(cuda_device, n_max):
+@pytest.mark.parametrize("n_max", [1200, 500, 20000],
+                         ids=["two_launches", "one_launch", "long_slabs"])
+def test_graph_replay_of_fused_steps(cuda_device, schedule, n_max):
     """Several fused steps captured in one HIP graph and replayed three times,
     each replay from the same initial cache with eager work in between: every
     replay matches the oracle step by step (the kernels hold no memset and
     leave the workspace counters zero, so replays are independent).  At
-    n_max = 500 every slab is one segment and each step is a single launch."""
+    n_max = 500 every slab is one segment and each step is a single launch;
+    at 20000 the short batch of long slabs runs as two-wave ranges (the
+    library's schedule) or with dynamic units (the fixture's other mode)."""
     T = 4
     shape = workloads.custom("graph", B=3, h_q=16, h_kv=2, d_k=128, d_v=128, n_max=n_max,
                              steps=T)
