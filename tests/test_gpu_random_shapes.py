@@ -61,6 +61,31 @@ DECODE_CASES = _cases(36, 20261) + [
 STEP_CASES = _cases(12, 771)
 
 
+def _long_cases(n, seed):
+    """Short batches of long slabs: the wholly static plans at one or two
+    workgroups per CU, and (under the fixture's dynamic mode) dynamic units
+    on slabs longer than the two-wave form's 4608 rows."""
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        h_kv = rng.choice([1, 2, 4, 8])
+        G = rng.choice([1, 2, 4, 8, 16, 20, 32])
+        d_k, d_v = rng.choice(HEAD_DIMS), rng.choice(HEAD_DIMS)
+        B = rng.choice([1, 2, 3, 4, 6])
+        n_max = rng.choice([4609, 6000, 9000, 16384, 25000])
+        if B * h_kv * G * n_max * (d_k + d_v) > 1.2e8:
+            continue
+        lens = [rng.randint(0, n_max) for _ in range(B)]
+        lens[0] = n_max
+        out.append((f"long{len(out)}_B{B}_hkv{h_kv}_G{G}_dk{d_k}_dv{d_v}_n{n_max}",
+                    B, h_kv * G, h_kv, d_k, d_v, n_max, lens, 0))
+    return out
+
+
+DECODE_CASES += _long_cases(10, 4099)
+STEP_CASES += _long_cases(4, 4117)
+
+
 def say(msg):
     print(msg, flush=True)
 
